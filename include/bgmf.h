@@ -1,0 +1,160 @@
+/*
+ * bgmf.h — C ABI of the MI355X (gfx950) blocked SGD matrix factorisation
+ * library (BGMF: block-based GPU matrix factorisation).
+ *
+ * Problem (paper, Section 1, Eq. 1): a sparse matrix X in R^{n x m} is
+ * observed at entries x_ij; find U in R^{n x k}, V in R^{m x k} with
+ * X ~ U V^T by stochastic gradient descent on
+ *     sum over observed x_ij of (x_ij - u_i.v_j)^2 + beta (|u_i|^2 + |v_j|^2).
+ *
+ * Method (Eq. 4, Section 1.1, Algorithm 1): X is cut into a p x p grid of
+ * blocks; row-block R holds rows [ceil(R n/p), ceil((R+1) n/p)), column-block
+ * C holds columns [ceil(C m/p), ceil((C+1) m/p)); equivalently row i is in
+ * row-block floor(i p / n).  Stratum s is the set of blocks (b, (b+s) mod p),
+ * b = 0..p-1; its blocks share no row and no column, so they run in
+ * parallel.  One epoch visits strata s = 0, 1, ..., p-1 in that order, and in
+ * each block applies, rating by rating, the update of Eq. 2-3:
+ *     e  = x_ij - u_i.v_j
+ *     u_i <- u_i + alpha (e v_j - beta u_i)
+ *     v_j <- v_j + alpha (e u_i - beta v_j)      (old u_i on the right)
+ * This is the paper's update with its factor 2 folded into the step:
+ * alpha = 2 alpha_paper, beta = beta_paper / 2.
+ *
+ * Inside a block, ratings are taken in ascending row, ties in ascending
+ * input position (the order the caller passed them to bgmf_load_coo).  The
+ * per-block pass count is one (Section 1.3: one pass per block is the exact
+ * scheme).
+ *
+ * Conventions for every call:
+ *   - Return value: BGMF_OK (0) or a negative BGMF_E_* code; the message is
+ *     available from bgmf_last_error(handle).  Nothing aborts the process.
+ *   - On error the handle keeps its previous valid state, except that a
+ *     failed bgmf_load_coo leaves no ratings loaded.
+ *   - Host pointers are read (or written) only during the call; the library
+ *     keeps no caller pointer after returning.
+ *   - A handle is not thread-safe.  All device work is ordered on the
+ *     handle's stream (see bgmf_set_stream).  bgmf_epoch returns without
+ *     waiting; bgmf_rmse, bgmf_get_factors, bgmf_get_layout, bgmf_sync and
+ *     bgmf_get_timing wait for the stream.
+ *   - All floating point is IEEE binary32 except where stated.
+ */
+#ifndef BGMF_H
+#define BGMF_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes. */
+#define BGMF_OK            0
+#define BGMF_E_ARG        -1  /* invalid argument (size, null pointer, alpha/beta) */
+#define BGMF_E_STATE      -2  /* call not valid in the handle's current state */
+#define BGMF_E_RANGE      -3  /* a rating index outside [0,n) x [0,m) */
+#define BGMF_E_NONFINITE  -4  /* a rating value that is NaN or infinite */
+#define BGMF_E_NOMEM      -5  /* device or host allocation failed */
+#define BGMF_E_UNSUPPORTED -6 /* shape the kernels do not handle */
+#define BGMF_E_HIP        -7  /* a HIP runtime call failed */
+#define BGMF_E_TIMEOUT    -8  /* a device-side wait between strata exceeded its limit */
+
+typedef struct bgmf bgmf_t; /* opaque handle */
+
+/* Create a handle for an n x m matrix, factor width k and a p x p grid
+ * (Algorithm 1's I = J = p).  Allocates U (n x k) and V (m x k) on the
+ * current HIP device.
+ *   1 <= n, m < 2^31;  k a multiple of 16 in [16, 256];
+ *   1 <= p <= min(n, m, 65535);  ceil(n/p) <= 65536;  ceil(m/p) <= 16384.
+ * Returns NULL on error; the reason is bgmf_last_error(NULL) (per thread). */
+bgmf_t *bgmf_create(int64_t n, int64_t m, int32_t k, int32_t p);
+
+/* Release every resource of the handle (waits for its stream first).
+ * NULL is ignored. */
+void bgmf_destroy(bgmf_t *h);
+
+/* Message of the last failed call on h, or of the last failed bgmf_create on
+ * this thread when h is NULL.  Owned by the library; valid until the next
+ * call on the same handle (or thread). */
+const char *bgmf_last_error(const bgmf_t *h);
+
+/* Order all later device work of h on a caller-owned hipStream_t (for
+ * example PyTorch's current stream).  NULL selects the handle's own stream.
+ * The caller keeps ownership; the stream must outlive its use by h. */
+int bgmf_set_stream(bgmf_t *h, void *hip_stream);
+
+/* Copy initial factors from host memory: U is n x k, V is m x k, row-major
+ * fp32 (u_i = U[i*k .. i*k+k)).  Algorithm 1 starts from random factors;
+ * the caller draws them.  Synchronous. */
+int bgmf_set_factors(bgmf_t *h, const float *U, const float *V);
+
+/* Load nnz ratings given as host COO arrays (rows[e], cols[e], vals[e]),
+ * e = 0..nnz-1, and bucket them into the p x p grid (Eq. 4) on the device.
+ *   1 <= nnz < 2^31.  Indices outside [0,n) x [0,m) -> BGMF_E_RANGE;
+ *   non-finite values -> BGMF_E_NONFINITE.  Duplicate (i, j) pairs are
+ *   separate ratings.  Replaces any earlier ratings.  Synchronous. */
+int bgmf_load_coo(bgmf_t *h, const int32_t *rows, const int32_t *cols, const float *vals,
+                  int64_t nnz);
+
+/* One epoch (one CPU step of Algorithm 1 with one pass per block): strata
+ * s = 0..p-1 in order, every loaded rating updated exactly once (Eq. 2-3).
+ * alpha > 0 and beta >= 0, both finite.  Needs factors and ratings.
+ * Asynchronous on the handle's stream; a device-side failure is reported by
+ * the next synchronising call. */
+int bgmf_epoch(bgmf_t *h, float alpha, float beta);
+
+/* Root-mean-square error over all loaded ratings with the current factors:
+ * sqrt((1/nnz) sum_e (x_e - u_i.v_j)^2), dots in fp32, sum in fp64 (the
+ * whole-matrix RMSE of Algorithm 1's termination test).  Waits for the
+ * stream. */
+int bgmf_rmse(bgmf_t *h, double *out);
+
+/* Copy the current factors to host memory (row-major n x k and m x k).
+ * Either pointer may be NULL to skip it.  Waits for the stream. */
+int bgmf_get_factors(bgmf_t *h, float *U, float *V);
+
+/* Bucketing result, for bit-exact checks:
+ *   block_ptr[q], q = 0..p*p: number of ratings in slots < q, where slot
+ *     q = s*p + R is block (R, (R+s) mod p) of stratum s;
+ *   perm[t], t = 0..nnz-1: input position of the t-th rating in slot order,
+ *     each slot sorted by (row, input position).
+ * Either pointer may be NULL.  Waits for the stream. */
+int bgmf_get_layout(bgmf_t *h, int64_t *block_ptr, int32_t *perm);
+
+/* Wait for all work on the handle's stream and report any device-side
+ * failure of earlier asynchronous calls. */
+int bgmf_sync(bgmf_t *h);
+
+/* Device pointers of U (n x k) and V (m x k), row-major fp32, owned by the
+ * handle and valid until bgmf_destroy.  Either output may be NULL. */
+int bgmf_factor_ptrs(bgmf_t *h, float **U_dev, float **V_dev);
+
+/* Options (bgmf_set_option / bgmf_get_option). */
+#define BGMF_OPT_SCHEDULE      1 /* 0: one persistent launch per epoch whose waves
+                                    hand column-blocks over with device-side
+                                    flags (default); 1: one launch per stratum */
+#define BGMF_OPT_WAIT_LIMIT_US 2 /* limit of one device-side wait, microseconds
+                                    (default 10,000,000) */
+#define BGMF_OPT_XCD_REMAP     3 /* 1 (default): place neighbouring row-blocks on
+                                    the same XCD; 0: plain workgroup order */
+int bgmf_set_option(bgmf_t *h, int32_t option, int64_t value);
+int bgmf_get_option(const bgmf_t *h, int32_t option, int64_t *value);
+
+/* Timing of the most recent bgmf_epoch and bgmf_rmse, measured with HIP
+ * events on the handle's stream around their kernels, in milliseconds
+ * (NaN if not run yet).  Waits for the stream. */
+int bgmf_get_timing(bgmf_t *h, double *epoch_ms, double *rmse_ms);
+
+/* Serial-chain statistics of the loaded ratings, from the block sizes:
+ *   out[0] = largest column-block total  (max_C sum_R nnz(R, C))
+ *   out[1] = largest row-block total     (max_R sum_C nnz(R, C))
+ *   out[2] = sum over strata of the largest block of the stratum
+ *   out[3] = number of non-empty blocks
+ * Needs ratings. */
+int bgmf_chain_stats(bgmf_t *h, int64_t out[4]);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BGMF_H */

@@ -1,0 +1,251 @@
+"""Thin ctypes binding of libbgmf.so (the C ABI in include/bgmf.h).
+
+Every function here only marshals arguments; all work runs in the HIP
+library.  There is no fallback: if libbgmf.so is missing or cannot be
+loaded, importing this module raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libbgmf.so")
+
+BGMF_OK = 0
+BGMF_E_ARG = -1
+BGMF_E_STATE = -2
+BGMF_E_RANGE = -3
+BGMF_E_NONFINITE = -4
+BGMF_E_NOMEM = -5
+BGMF_E_UNSUPPORTED = -6
+BGMF_E_HIP = -7
+BGMF_E_TIMEOUT = -8
+
+BGMF_OPT_SCHEDULE = 1
+BGMF_OPT_WAIT_LIMIT_US = 2
+BGMF_OPT_XCD_REMAP = 3
+
+EXPORTED = (
+    "bgmf_create", "bgmf_destroy", "bgmf_last_error", "bgmf_set_stream", "bgmf_set_factors",
+    "bgmf_load_coo", "bgmf_epoch", "bgmf_rmse", "bgmf_get_factors", "bgmf_get_layout",
+    "bgmf_sync", "bgmf_factor_ptrs", "bgmf_set_option", "bgmf_get_option", "bgmf_get_timing",
+    "bgmf_chain_stats",
+)
+
+
+class BgmfError(RuntimeError):
+    def __init__(self, code: int, message: str):
+        super().__init__(f"[{code}] {message}")
+        self.code = code
+
+
+def _load() -> ctypes.CDLL:
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() or "
+                          "python -m paper_2304_13724_amd.build")
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, I64, I32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32
+    F32, c_int = ctypes.c_float, ctypes.c_int
+    sig = {
+        "bgmf_create": ([I64, I64, I32, I32], vp),
+        "bgmf_destroy": ([vp], None),
+        "bgmf_last_error": ([vp], ctypes.c_char_p),
+        "bgmf_set_stream": ([vp, vp], c_int),
+        "bgmf_set_factors": ([vp, vp, vp], c_int),
+        "bgmf_load_coo": ([vp, vp, vp, vp, I64], c_int),
+        "bgmf_epoch": ([vp, F32, F32], c_int),
+        "bgmf_rmse": ([vp, ctypes.POINTER(ctypes.c_double)], c_int),
+        "bgmf_get_factors": ([vp, vp, vp], c_int),
+        "bgmf_get_layout": ([vp, vp, vp], c_int),
+        "bgmf_sync": ([vp], c_int),
+        "bgmf_factor_ptrs": ([vp, ctypes.POINTER(vp), ctypes.POINTER(vp)], c_int),
+        "bgmf_set_option": ([vp, I32, I64], c_int),
+        "bgmf_get_option": ([vp, I32, ctypes.POINTER(I64)], c_int),
+        "bgmf_get_timing": ([vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)],
+                            c_int),
+        "bgmf_chain_stats": ([vp, vp], c_int),
+    }
+    for name, (args, res) in sig.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = res
+    return lib
+
+
+_lib = _load()
+
+
+def _ptr(a: np.ndarray):
+    assert a.flags["C_CONTIGUOUS"]
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _check(h, rc: int):
+    if rc != BGMF_OK:
+        msg = _lib.bgmf_last_error(h)
+        raise BgmfError(rc, msg.decode() if msg else "")
+
+
+# --- functions with the C names (argument marshalling only) -----------------
+
+def bgmf_create(n: int, m: int, k: int, p: int):
+    h = _lib.bgmf_create(int(n), int(m), int(k), int(p))
+    if not h:
+        msg = _lib.bgmf_last_error(None)
+        raise BgmfError(BGMF_E_ARG, msg.decode() if msg else "bgmf_create failed")
+    return h
+
+
+def bgmf_destroy(h) -> None:
+    _lib.bgmf_destroy(h)
+
+
+def bgmf_last_error(h) -> str:
+    msg = _lib.bgmf_last_error(h)
+    return msg.decode() if msg else ""
+
+
+def bgmf_set_stream(h, stream) -> None:
+    """``stream``: an integer hipStream_t (e.g. torch.cuda.current_stream().cuda_stream)
+    or None for the handle's own stream."""
+    _check(h, _lib.bgmf_set_stream(h, ctypes.c_void_p(int(stream)) if stream else None))
+
+
+def bgmf_set_factors(h, U: np.ndarray, V: np.ndarray) -> None:
+    U = np.ascontiguousarray(U, dtype=np.float32)
+    V = np.ascontiguousarray(V, dtype=np.float32)
+    _check(h, _lib.bgmf_set_factors(h, _ptr(U), _ptr(V)))
+
+
+def bgmf_load_coo(h, rows, cols, vals) -> None:
+    rows = np.ascontiguousarray(rows, dtype=np.int32)
+    cols = np.ascontiguousarray(cols, dtype=np.int32)
+    vals = np.ascontiguousarray(vals, dtype=np.float32)
+    if not (rows.shape == cols.shape == vals.shape and rows.ndim == 1):
+        raise ValueError("rows, cols and vals must be 1-D arrays of one length")
+    _check(h, _lib.bgmf_load_coo(h, _ptr(rows), _ptr(cols), _ptr(vals), rows.shape[0]))
+
+
+def bgmf_epoch(h, alpha: float, beta: float) -> None:
+    _check(h, _lib.bgmf_epoch(h, float(alpha), float(beta)))
+
+
+def bgmf_rmse(h) -> float:
+    out = ctypes.c_double(math.nan)
+    _check(h, _lib.bgmf_rmse(h, ctypes.byref(out)))
+    return out.value
+
+
+def bgmf_get_factors(h, n: int, m: int, k: int):
+    U = np.empty((n, k), dtype=np.float32)
+    V = np.empty((m, k), dtype=np.float32)
+    _check(h, _lib.bgmf_get_factors(h, _ptr(U), _ptr(V)))
+    return U, V
+
+
+def bgmf_get_layout(h, p: int, nnz: int):
+    block_ptr = np.empty(p * p + 1, dtype=np.int64)
+    perm = np.empty(max(nnz, 1), dtype=np.int32)
+    _check(h, _lib.bgmf_get_layout(h, _ptr(block_ptr), _ptr(perm)))
+    return block_ptr, perm[:nnz]
+
+
+def bgmf_sync(h) -> None:
+    _check(h, _lib.bgmf_sync(h))
+
+
+def bgmf_factor_ptrs(h):
+    u, v = ctypes.c_void_p(), ctypes.c_void_p()
+    _check(h, _lib.bgmf_factor_ptrs(h, ctypes.byref(u), ctypes.byref(v)))
+    return u.value, v.value
+
+
+def bgmf_set_option(h, option: int, value: int) -> None:
+    _check(h, _lib.bgmf_set_option(h, int(option), int(value)))
+
+
+def bgmf_get_option(h, option: int) -> int:
+    out = ctypes.c_int64()
+    _check(h, _lib.bgmf_get_option(h, int(option), ctypes.byref(out)))
+    return out.value
+
+
+def bgmf_get_timing(h):
+    e, r = ctypes.c_double(), ctypes.c_double()
+    _check(h, _lib.bgmf_get_timing(h, ctypes.byref(e), ctypes.byref(r)))
+    return e.value, r.value
+
+
+def bgmf_chain_stats(h):
+    out = np.zeros(4, dtype=np.int64)
+    _check(h, _lib.bgmf_chain_stats(h, _ptr(out)))
+    return out
+
+
+# --- convenience wrapper -----------------------------------------------------
+
+class Model:
+    """Owns one handle: ``Model(n, m, k, p)``; see include/bgmf.h."""
+
+    def __init__(self, n: int, m: int, k: int, p: int):
+        self.n, self.m, self.k, self.p = int(n), int(m), int(k), int(p)
+        self.nnz = 0
+        self.h = bgmf_create(n, m, k, p)
+
+    def close(self):
+        if self.h:
+            bgmf_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    def set_stream(self, stream):
+        bgmf_set_stream(self.h, stream)
+
+    def set_factors(self, U, V):
+        bgmf_set_factors(self.h, U, V)
+
+    def load_coo(self, rows, cols, vals):
+        bgmf_load_coo(self.h, rows, cols, vals)
+        self.nnz = int(np.asarray(rows).shape[0])
+
+    def epoch(self, alpha: float, beta: float):
+        bgmf_epoch(self.h, alpha, beta)
+
+    def rmse(self) -> float:
+        return bgmf_rmse(self.h)
+
+    def get_factors(self):
+        return bgmf_get_factors(self.h, self.n, self.m, self.k)
+
+    def get_layout(self):
+        return bgmf_get_layout(self.h, self.p, self.nnz)
+
+    def sync(self):
+        bgmf_sync(self.h)
+
+    def set_option(self, option: int, value: int):
+        bgmf_set_option(self.h, option, value)
+
+    def get_option(self, option: int) -> int:
+        return bgmf_get_option(self.h, option)
+
+    def timing(self):
+        return bgmf_get_timing(self.h)
+
+    def chain_stats(self):
+        return bgmf_chain_stats(self.h)

@@ -1,0 +1,521 @@
+// Host side of the C ABI declared in include/bgmf.h: handle state, argument
+// validation, device memory, and the order of kernel launches on the
+// handle's stream.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "../../include/bgmf.h"
+#include "bgmf_internal.h"
+
+using namespace bgmfk;
+
+struct bgmf {
+  int64_t n = 0, m = 0;
+  int32_t k = 0, p = 0, kp = 0;
+  int device = 0;
+  int cus = 0;
+  hipStream_t own_stream = nullptr;
+  hipStream_t stream = nullptr;
+  float *U = nullptr, *V = nullptr;
+  // ratings layout
+  int64_t nnz = 0;
+  int64_t *block_ptr = nullptr, *wblock_ptr = nullptr;
+  int32_t *perm = nullptr;
+  uint2 *rec = nullptr;
+  int64_t *flags = nullptr;
+  int32_t *err = nullptr;
+  double *partials = nullptr, *d_rmse = nullptr;
+  int64_t epochs_done = 0;
+  bool factors_set = false, loaded = false;
+  // launch shape
+  int cols_max = 0;
+  int wpg = kWavesPerGroup;
+  size_t lds_bytes = 0;
+  size_t lds_limit = 0;
+  bool coop_ok = false;
+  // options
+  int64_t schedule = 0, wait_us = 10000000, xcd_remap = 1;
+  // timing
+  hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
+  bool epoch_timed = false, rmse_timed = false;
+  int64_t chain[4] = {0, 0, 0, 0};
+  std::string msg;
+};
+
+namespace {
+
+thread_local std::string g_create_error;
+
+int fail(bgmf_t *h, int code, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  if (h) h->msg = buf;
+  else g_create_error = buf;
+  return code;
+}
+
+#define HIP_TRY(h, call)                                                                   \
+  do {                                                                                     \
+    hipError_t e_ = (call);                                                                \
+    if (e_ != hipSuccess)                                                                  \
+      return fail((h), e_ == hipErrorOutOfMemory ? BGMF_E_NOMEM : BGMF_E_HIP, "%s: %s",    \
+                  #call, hipGetErrorString(e_));                                           \
+  } while (0)
+
+void free_layout(bgmf_t *h) {
+  hipFree(h->block_ptr);
+  hipFree(h->wblock_ptr);
+  hipFree(h->perm);
+  hipFree(h->rec);
+  h->block_ptr = h->wblock_ptr = nullptr;
+  h->perm = nullptr;
+  h->rec = nullptr;
+  h->nnz = 0;
+  h->loaded = false;
+}
+
+// Device-side error word: read, report, clear.  After a failed wait the
+// progress words no longer describe a completed epoch; they are reset so
+// that later epochs start cleanly (the factors hold a partial epoch).
+int check_device_error(bgmf_t *h) {
+  int32_t e = 0;
+  HIP_TRY(h, hipMemcpyAsync(&e, h->err, sizeof e, hipMemcpyDeviceToHost, h->stream));
+  HIP_TRY(h, hipStreamSynchronize(h->stream));
+  if (e == 0) return BGMF_OK;
+  std::vector<int64_t> fl((size_t)h->p * kFlagStride, h->epochs_done * (int64_t)h->p);
+  HIP_TRY(h, hipMemcpyAsync(h->flags, fl.data(), fl.size() * sizeof(int64_t),
+                            hipMemcpyHostToDevice, h->stream));
+  HIP_TRY(h, hipMemsetAsync(h->err, 0, sizeof(int32_t), h->stream));
+  HIP_TRY(h, hipStreamSynchronize(h->stream));
+  return fail(h, BGMF_E_TIMEOUT,
+              "a device-side wait between strata exceeded its limit (%lld us); the last epoch "
+              "is incomplete",
+              (long long)h->wait_us);
+}
+
+int sync_checked(bgmf_t *h) {
+  HIP_TRY(h, hipStreamSynchronize(h->stream));
+  return check_device_error(h);
+}
+
+}  // namespace
+
+extern "C" {
+
+bgmf_t *bgmf_create(int64_t n, int64_t m, int32_t k, int32_t p) {
+  if (n < 1 || m < 1 || n >= (1ll << 31) || m >= (1ll << 31)) {
+    fail(nullptr, BGMF_E_ARG, "n and m must be in [1, 2^31): n=%lld m=%lld", (long long)n,
+         (long long)m);
+    return nullptr;
+  }
+  if (k < 16 || k > 256 || k % 16 != 0) {
+    fail(nullptr, BGMF_E_ARG, "k must be a multiple of 16 in [16, 256]: k=%d", k);
+    return nullptr;
+  }
+  if (p < 1 || p > 8192 || p > n || p > m) {
+    fail(nullptr, BGMF_E_ARG, "p must be in [1, min(n, m, 8192)]: p=%d", p);
+    return nullptr;
+  }
+  if ((n + p - 1) / p > 65536 || (m + p - 1) / p > (1 << kColBits)) {
+    fail(nullptr, BGMF_E_ARG, "blocks too large: ceil(n/p)=%lld (max 65536), ceil(m/p)=%lld (max %d)",
+         (long long)((n + p - 1) / p), (long long)((m + p - 1) / p), 1 << kColBits);
+    return nullptr;
+  }
+  bgmf_t *h = new (std::nothrow) bgmf();
+  if (!h) {
+    fail(nullptr, BGMF_E_NOMEM, "out of host memory");
+    return nullptr;
+  }
+  h->n = n;
+  h->m = m;
+  h->k = k;
+  h->p = p;
+  h->kp = 16;
+  while (h->kp < k) h->kp <<= 1;
+  const Grid G{n, m, p};
+  for (int64_t C = 0; C < p; ++C)
+    h->cols_max = std::max<int>(h->cols_max, (int)(G.col_start(C + 1) - G.col_start(C)));
+
+  auto bail = [&](hipError_t e, const char *what) -> bgmf_t * {
+    fail(nullptr, e == hipErrorOutOfMemory ? BGMF_E_NOMEM : BGMF_E_HIP, "%s: %s", what,
+         hipGetErrorString(e));
+    bgmf_destroy(h);
+    return nullptr;
+  };
+  hipError_t e;
+  if ((e = hipGetDevice(&h->device)) != hipSuccess) return bail(e, "hipGetDevice");
+  int lds_max = 0;
+  if ((e = hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, h->device)) !=
+      hipSuccess)
+    return bail(e, "hipDeviceGetAttribute");
+  if ((e = hipDeviceGetAttribute(&h->cus, hipDeviceAttributeMultiprocessorCount, h->device)) !=
+      hipSuccess)
+    return bail(e, "hipDeviceGetAttribute");
+  h->lds_limit = (size_t)lds_max;
+  // the widest workgroup (4, 2 or 1 waves) whose column slices fit in LDS
+  const size_t slice = (size_t)(h->cols_max + 1) * h->kp * sizeof(float);
+  h->wpg = kWavesPerGroup;
+  while (h->wpg > 1 && h->wpg * slice > h->lds_limit) h->wpg >>= 1;
+  h->lds_bytes = h->wpg * slice;
+  if (h->lds_bytes > h->lds_limit) {
+    fail(nullptr, BGMF_E_UNSUPPORTED,
+         "one column-block slice ((%d + 1) columns x %d floats = %zu bytes) exceeds the %zu "
+         "bytes of LDS per workgroup",
+         h->cols_max, h->kp, slice, h->lds_limit);
+    bgmf_destroy(h);
+    return nullptr;
+  }
+  if ((e = sgd_set_lds_limit(h->kp, h->k != h->kp, h->lds_bytes)) != hipSuccess)
+    return bail(e, "hipFuncSetAttribute");
+  int per_cu = 0;
+  if ((e = sgd_occupancy(h->kp, h->k != h->kp, h->wpg, h->lds_bytes, &per_cu)) != hipSuccess)
+    return bail(e, "hipOccupancyMaxActiveBlocksPerMultiprocessor");
+  const int64_t groups = (p + h->wpg - 1) / h->wpg;
+  h->coop_ok = (int64_t)per_cu * h->cus >= groups;
+  if ((e = hipStreamCreateWithFlags(&h->own_stream, hipStreamNonBlocking)) != hipSuccess)
+    return bail(e, "hipStreamCreate");
+  h->stream = h->own_stream;
+  for (auto &ev : h->ev)
+    if ((e = hipEventCreate(&ev)) != hipSuccess) return bail(e, "hipEventCreate");
+  // one spare row after U absorbs the padding steps of the sweep
+  if ((e = hipMalloc(&h->U, (size_t)(n + 1) * k * sizeof(float))) != hipSuccess)
+    return bail(e, "hipMalloc(U)");
+  if ((e = hipMalloc(&h->V, (size_t)m * k * sizeof(float))) != hipSuccess)
+    return bail(e, "hipMalloc(V)");
+  if ((e = hipMalloc(&h->flags, (size_t)p * kFlagStride * sizeof(int64_t))) != hipSuccess)
+    return bail(e, "hipMalloc(flags)");
+  if ((e = hipMalloc(&h->err, sizeof(int32_t))) != hipSuccess) return bail(e, "hipMalloc(err)");
+  if ((e = hipMalloc(&h->partials, rmse_partials_count(p) * sizeof(double))) != hipSuccess)
+    return bail(e, "hipMalloc(partials)");
+  if ((e = hipMalloc(&h->d_rmse, sizeof(double))) != hipSuccess)
+    return bail(e, "hipMalloc(rmse)");
+  if ((e = hipMemset(h->flags, 0, (size_t)p * kFlagStride * sizeof(int64_t))) != hipSuccess)
+    return bail(e, "hipMemset");
+  if ((e = hipMemset(h->err, 0, sizeof(int32_t))) != hipSuccess) return bail(e, "hipMemset");
+  if ((e = hipMemset(h->U, 0, (size_t)(n + 1) * k * sizeof(float))) != hipSuccess)
+    return bail(e, "hipMemset");
+  if ((e = hipMemset(h->V, 0, (size_t)m * k * sizeof(float))) != hipSuccess)
+    return bail(e, "hipMemset");
+  return h;
+}
+
+void bgmf_destroy(bgmf_t *h) {
+  if (!h) return;
+  if (h->stream) hipStreamSynchronize(h->stream);
+  free_layout(h);
+  hipFree(h->U);
+  hipFree(h->V);
+  hipFree(h->flags);
+  hipFree(h->err);
+  hipFree(h->partials);
+  hipFree(h->d_rmse);
+  for (auto &ev : h->ev)
+    if (ev) hipEventDestroy(ev);
+  if (h->own_stream) hipStreamDestroy(h->own_stream);
+  delete h;
+}
+
+const char *bgmf_last_error(const bgmf_t *h) {
+  return h ? h->msg.c_str() : g_create_error.c_str();
+}
+
+int bgmf_set_stream(bgmf_t *h, void *hip_stream) {
+  if (!h) return BGMF_E_ARG;
+  hipStream_t next = hip_stream ? static_cast<hipStream_t>(hip_stream) : h->own_stream;
+  if (next != h->stream) {
+    // work already queued on the old stream finishes before later work
+    HIP_TRY(h, hipStreamSynchronize(h->stream));
+    h->stream = next;
+  }
+  return BGMF_OK;
+}
+
+int bgmf_set_factors(bgmf_t *h, const float *U, const float *V) {
+  if (!h) return BGMF_E_ARG;
+  if (!U || !V) return fail(h, BGMF_E_ARG, "bgmf_set_factors: null pointer");
+  for (int64_t x = 0, cnt = h->n * h->k; x < cnt; ++x)
+    if (!std::isfinite(U[x])) return fail(h, BGMF_E_NONFINITE, "U[%lld] is not finite", (long long)x);
+  for (int64_t x = 0, cnt = h->m * h->k; x < cnt; ++x)
+    if (!std::isfinite(V[x])) return fail(h, BGMF_E_NONFINITE, "V[%lld] is not finite", (long long)x);
+  HIP_TRY(h, hipMemcpyAsync(h->U, U, (size_t)h->n * h->k * sizeof(float), hipMemcpyHostToDevice,
+                            h->stream));
+  HIP_TRY(h, hipMemcpyAsync(h->V, V, (size_t)h->m * h->k * sizeof(float), hipMemcpyHostToDevice,
+                            h->stream));
+  HIP_TRY(h, hipStreamSynchronize(h->stream));
+  h->factors_set = true;
+  return BGMF_OK;
+}
+
+int bgmf_load_coo(bgmf_t *h, const int32_t *rows, const int32_t *cols, const float *vals,
+                  int64_t nnz) {
+  if (!h) return BGMF_E_ARG;
+  if (!rows || !cols || !vals) return fail(h, BGMF_E_ARG, "bgmf_load_coo: null pointer");
+  if (nnz < 1 || nnz >= (1ll << 31))
+    return fail(h, BGMF_E_ARG, "nnz must be in [1, 2^31): %lld", (long long)nnz);
+  for (int64_t e = 0; e < nnz; ++e) {
+    if (rows[e] < 0 || rows[e] >= h->n || cols[e] < 0 || cols[e] >= h->m)
+      return fail(h, BGMF_E_RANGE, "rating %lld at (%d, %d) is outside the %lld x %lld matrix",
+                  (long long)e, rows[e], cols[e], (long long)h->n, (long long)h->m);
+    if (!std::isfinite(vals[e]))
+      return fail(h, BGMF_E_NONFINITE, "rating %lld has a non-finite value", (long long)e);
+  }
+  HIP_TRY(h, hipStreamSynchronize(h->stream));
+  free_layout(h);
+
+  const int64_t slots = (int64_t)h->p * h->p;
+  int32_t *d_rows = nullptr, *d_cols = nullptr;
+  float *d_vals = nullptr;
+  void *scratch = nullptr;
+  const size_t scratch_bytes = bucket_scratch_bytes(nnz, h->p);
+  int rc = BGMF_OK;
+  auto cleanup = [&]() {
+    hipFree(d_rows);
+    hipFree(d_cols);
+    hipFree(d_vals);
+    hipFree(scratch);
+  };
+#define LOAD_TRY(call)                                                                     \
+  do {                                                                                     \
+    hipError_t e_ = (call);                                                                \
+    if (e_ != hipSuccess) {                                                                \
+      rc = fail(h, e_ == hipErrorOutOfMemory ? BGMF_E_NOMEM : BGMF_E_HIP, "%s: %s", #call, \
+                hipGetErrorString(e_));                                                    \
+      cleanup();                                                                           \
+      free_layout(h);                                                                      \
+      return rc;                                                                           \
+    }                                                                                      \
+  } while (0)
+  LOAD_TRY(hipMalloc(&d_rows, (size_t)nnz * sizeof(int32_t)));
+  LOAD_TRY(hipMalloc(&d_cols, (size_t)nnz * sizeof(int32_t)));
+  LOAD_TRY(hipMalloc(&d_vals, (size_t)nnz * sizeof(float)));
+  LOAD_TRY(hipMalloc(&scratch, scratch_bytes));
+  LOAD_TRY(hipMalloc(&h->block_ptr, (size_t)(slots + 1) * sizeof(int64_t)));
+  LOAD_TRY(hipMalloc(&h->wblock_ptr, (size_t)(slots + 1) * sizeof(int64_t)));
+  LOAD_TRY(hipMalloc(&h->perm, (size_t)nnz * sizeof(int32_t)));
+  LOAD_TRY(hipMalloc(&h->rec, (size_t)(nnz + kRecPad) * sizeof(uint2)));
+  LOAD_TRY(hipMemcpyAsync(d_rows, rows, (size_t)nnz * sizeof(int32_t), hipMemcpyHostToDevice,
+                          h->stream));
+  LOAD_TRY(hipMemcpyAsync(d_cols, cols, (size_t)nnz * sizeof(int32_t), hipMemcpyHostToDevice,
+                          h->stream));
+  LOAD_TRY(hipMemcpyAsync(d_vals, vals, (size_t)nnz * sizeof(float), hipMemcpyHostToDevice,
+                          h->stream));
+  BucketOut out{h->block_ptr, h->wblock_ptr, h->perm, h->rec};
+  LOAD_TRY(hipMemsetAsync(h->err, 0, sizeof(int32_t), h->stream));
+  LOAD_TRY(bucket(d_rows, d_cols, d_vals, nnz, h->n, h->m, h->p, /*flag_v_reload=*/false, scratch,
+                  scratch_bytes, out, h->err, h->stream));
+  LOAD_TRY(hipStreamSynchronize(h->stream));
+  cleanup();
+#undef LOAD_TRY
+  int32_t derr = 0;
+  HIP_TRY(h, hipMemcpy(&derr, h->err, sizeof derr, hipMemcpyDeviceToHost));
+
+  // serial-chain statistics from the block sizes
+  std::vector<int64_t> bp((size_t)slots + 1), wbp((size_t)slots + 1);
+  HIP_TRY(h, hipMemcpy(bp.data(), h->block_ptr, bp.size() * sizeof(int64_t),
+                       hipMemcpyDeviceToHost));
+  HIP_TRY(h, hipMemcpy(wbp.data(), h->wblock_ptr, wbp.size() * sizeof(int64_t),
+                       hipMemcpyDeviceToHost));
+  // the sweep trusts these offsets: check them before any epoch may run
+  bool ok = derr == 0 && bp[0] == 0 && wbp[0] == 0 && bp[slots] == nnz && wbp[slots] == nnz;
+  for (int64_t q = 0; ok && q < slots; ++q) ok = bp[q] <= bp[q + 1] && wbp[q] <= wbp[q + 1];
+  for (int64_t b = 0; ok && b < h->p; ++b)
+    for (int64_t s2 = 0; ok && s2 < h->p; ++s2)
+      ok = wbp[b * h->p + s2 + 1] - wbp[b * h->p + s2] == bp[s2 * h->p + b + 1] - bp[s2 * h->p + b];
+  if (!ok) {
+    hipMemset(h->err, 0, sizeof(int32_t));
+    free_layout(h);
+    return fail(h, BGMF_E_HIP, "internal error: the device bucketing produced an inconsistent layout");
+  }
+  std::vector<int64_t> colsum(h->p, 0), rowsum(h->p, 0);
+  int64_t barrier = 0, nonempty = 0;
+  for (int64_t s = 0; s < h->p; ++s) {
+    int64_t mx = 0;
+    for (int64_t R = 0; R < h->p; ++R) {
+      const int64_t c = bp[s * h->p + R + 1] - bp[s * h->p + R];
+      colsum[(R + s) % h->p] += c;
+      rowsum[R] += c;
+      mx = std::max(mx, c);
+      nonempty += c > 0;
+    }
+    barrier += mx;
+  }
+  h->chain[0] = *std::max_element(colsum.begin(), colsum.end());
+  h->chain[1] = *std::max_element(rowsum.begin(), rowsum.end());
+  h->chain[2] = barrier;
+  h->chain[3] = nonempty;
+
+  HIP_TRY(h, hipMemsetAsync(h->flags, 0, (size_t)h->p * kFlagStride * sizeof(int64_t), h->stream));
+  HIP_TRY(h, hipStreamSynchronize(h->stream));
+  h->epochs_done = 0;
+  h->nnz = nnz;
+  h->loaded = true;
+  return BGMF_OK;
+}
+
+int bgmf_epoch(bgmf_t *h, float alpha, float beta) {
+  if (!h) return BGMF_E_ARG;
+  if (!std::isfinite(alpha) || !(alpha > 0.0f) || !std::isfinite(beta) || beta < 0.0f)
+    return fail(h, BGMF_E_ARG, "alpha must be finite and > 0, beta finite and >= 0");
+  if (!h->loaded) return fail(h, BGMF_E_STATE, "bgmf_epoch: no ratings loaded");
+  if (!h->factors_set) return fail(h, BGMF_E_STATE, "bgmf_epoch: factors not set");
+  SgdParams P{};
+  P.U = h->U;
+  P.V = h->V;
+  P.rec = h->rec;
+  P.wblock_ptr = h->wblock_ptr;
+  P.flags = h->flags;
+  P.err = h->err;
+  P.n = h->n;
+  P.m = h->m;
+  P.k = h->k;
+  P.p = h->p;
+  P.cols_max = h->cols_max;
+  P.g_base = h->epochs_done * (int64_t)h->p;
+  P.wait_ticks = h->wait_us * 100;  // s_memrealtime runs at 100 MHz
+  P.alpha = alpha;
+  P.beta = beta;
+  P.xcd_remap = (int32_t)h->xcd_remap;
+  const bool persistent = h->schedule == 0 && h->coop_ok;
+  HIP_TRY(h, hipEventRecord(h->ev[0], h->stream));
+  if (persistent) {
+    P.s_begin = 0;
+    P.s_end = h->p;
+    HIP_TRY(h, launch_sgd(P, h->kp, h->wpg, true, h->lds_bytes, h->stream));
+  } else {
+    for (int32_t s = 0; s < h->p; ++s) {
+      P.s_begin = s;
+      P.s_end = s + 1;
+      HIP_TRY(h, launch_sgd(P, h->kp, h->wpg, false, h->lds_bytes, h->stream));
+    }
+  }
+  HIP_TRY(h, hipEventRecord(h->ev[1], h->stream));
+  h->epoch_timed = true;
+  h->epochs_done += 1;
+  return BGMF_OK;
+}
+
+int bgmf_rmse(bgmf_t *h, double *out) {
+  if (!h) return BGMF_E_ARG;
+  if (!out) return fail(h, BGMF_E_ARG, "bgmf_rmse: null output");
+  if (!h->loaded) return fail(h, BGMF_E_STATE, "bgmf_rmse: no ratings loaded");
+  if (!h->factors_set) return fail(h, BGMF_E_STATE, "bgmf_rmse: factors not set");
+  HIP_TRY(h, hipEventRecord(h->ev[2], h->stream));
+  HIP_TRY(h, launch_rmse(h->rec, h->wblock_ptr, h->U, h->V, h->n, h->m, h->k, h->p, h->nnz,
+                         h->partials, h->d_rmse, h->stream));
+  HIP_TRY(h, hipEventRecord(h->ev[3], h->stream));
+  h->rmse_timed = true;
+  double r = 0.0;
+  HIP_TRY(h, hipMemcpyAsync(&r, h->d_rmse, sizeof r, hipMemcpyDeviceToHost, h->stream));
+  int rc = sync_checked(h);
+  if (rc != BGMF_OK) return rc;
+  *out = r;
+  return BGMF_OK;
+}
+
+int bgmf_get_factors(bgmf_t *h, float *U, float *V) {
+  if (!h) return BGMF_E_ARG;
+  if (U)
+    HIP_TRY(h, hipMemcpyAsync(U, h->U, (size_t)h->n * h->k * sizeof(float), hipMemcpyDeviceToHost,
+                              h->stream));
+  if (V)
+    HIP_TRY(h, hipMemcpyAsync(V, h->V, (size_t)h->m * h->k * sizeof(float), hipMemcpyDeviceToHost,
+                              h->stream));
+  return sync_checked(h);
+}
+
+int bgmf_get_layout(bgmf_t *h, int64_t *block_ptr, int32_t *perm) {
+  if (!h) return BGMF_E_ARG;
+  if (!h->loaded) return fail(h, BGMF_E_STATE, "bgmf_get_layout: no ratings loaded");
+  if (block_ptr)
+    HIP_TRY(h, hipMemcpyAsync(block_ptr, h->block_ptr,
+                              (size_t)((int64_t)h->p * h->p + 1) * sizeof(int64_t),
+                              hipMemcpyDeviceToHost, h->stream));
+  if (perm)
+    HIP_TRY(h, hipMemcpyAsync(perm, h->perm, (size_t)h->nnz * sizeof(int32_t),
+                              hipMemcpyDeviceToHost, h->stream));
+  return sync_checked(h);
+}
+
+int bgmf_sync(bgmf_t *h) {
+  if (!h) return BGMF_E_ARG;
+  return sync_checked(h);
+}
+
+int bgmf_factor_ptrs(bgmf_t *h, float **U_dev, float **V_dev) {
+  if (!h) return BGMF_E_ARG;
+  if (U_dev) *U_dev = h->U;
+  if (V_dev) *V_dev = h->V;
+  return BGMF_OK;
+}
+
+int bgmf_set_option(bgmf_t *h, int32_t option, int64_t value) {
+  if (!h) return BGMF_E_ARG;
+  switch (option) {
+    case BGMF_OPT_SCHEDULE:
+      if (value != 0 && value != 1) return fail(h, BGMF_E_ARG, "schedule must be 0 or 1");
+      h->schedule = value;
+      return BGMF_OK;
+    case BGMF_OPT_WAIT_LIMIT_US:
+      if (value < 0) return fail(h, BGMF_E_ARG, "wait limit must be >= 0");
+      h->wait_us = value;
+      return BGMF_OK;
+    case BGMF_OPT_XCD_REMAP:
+      if (value != 0 && value != 1) return fail(h, BGMF_E_ARG, "xcd remap must be 0 or 1");
+      h->xcd_remap = value;
+      return BGMF_OK;
+    default:
+      return fail(h, BGMF_E_ARG, "unknown option %d", option);
+  }
+}
+
+int bgmf_get_option(const bgmf_t *h, int32_t option, int64_t *value) {
+  if (!h || !value) return BGMF_E_ARG;
+  switch (option) {
+    case BGMF_OPT_SCHEDULE: *value = h->schedule; return BGMF_OK;
+    case BGMF_OPT_WAIT_LIMIT_US: *value = h->wait_us; return BGMF_OK;
+    case BGMF_OPT_XCD_REMAP: *value = h->xcd_remap; return BGMF_OK;
+    default: return BGMF_E_ARG;
+  }
+}
+
+int bgmf_get_timing(bgmf_t *h, double *epoch_ms, double *rmse_ms) {
+  if (!h) return BGMF_E_ARG;
+  int rc = sync_checked(h);
+  if (rc != BGMF_OK) return rc;
+  float ms = 0.0f;
+  if (epoch_ms) {
+    *epoch_ms = NAN;
+    if (h->epoch_timed) {
+      HIP_TRY(h, hipEventElapsedTime(&ms, h->ev[0], h->ev[1]));
+      *epoch_ms = ms;
+    }
+  }
+  if (rmse_ms) {
+    *rmse_ms = NAN;
+    if (h->rmse_timed) {
+      HIP_TRY(h, hipEventElapsedTime(&ms, h->ev[2], h->ev[3]));
+      *rmse_ms = ms;
+    }
+  }
+  return BGMF_OK;
+}
+
+int bgmf_chain_stats(bgmf_t *h, int64_t out[4]) {
+  if (!h || !out) return BGMF_E_ARG;
+  if (!h->loaded) return fail(h, BGMF_E_STATE, "bgmf_chain_stats: no ratings loaded");
+  for (int i = 0; i < 4; ++i) out[i] = h->chain[i];
+  return BGMF_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,86 @@
+// Internal declarations shared by the HIP sources of libbgmf (gfx950 only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace bgmfk {
+
+// ---------------------------------------------------------------------------
+// Rating record (8 bytes), stored contiguously per row-block ("wave stream"):
+//   .x = local row (16 bits) | local column << 16 (14 bits) | flags (2 bits)
+//   .y = rating value (fp32 bits)
+// Local indices are relative to the block's first row / first column.
+// ---------------------------------------------------------------------------
+constexpr int kRowBits = 16;
+constexpr int kColShift = 16;
+constexpr int kColBits = 14;
+constexpr uint32_t kRowMask = (1u << kRowBits) - 1u;
+constexpr uint32_t kColMask = (1u << kColBits) - 1u;
+constexpr uint32_t kFlagVReload = 1u << 30;  // v_j was updated 2..kPrefetch-1 ratings ago
+constexpr int kPrefetch = 16;                // prefetch distance of factor rows (ratings)
+constexpr int kRecPad = 256;                 // padding records after the last stream
+
+// Block geometry of the p x p grid: row-block R holds rows
+// [ceil(R n / p), ceil((R+1) n / p)), i.e. row i is in floor(i p / n).
+struct Grid {
+  int64_t n, m;
+  int32_t p;
+  __host__ __device__ __forceinline__ int64_t row_start(int64_t R) const {
+    return (R * n + p - 1) / p;
+  }
+  __host__ __device__ __forceinline__ int64_t col_start(int64_t C) const {
+    return (C * m + p - 1) / p;
+  }
+};
+
+// Arguments of the SGD sweep kernels.
+struct SgdParams {
+  float *U;                  // n x k, plus one spare row (index n)
+  float *V;                  // m x k
+  const uint2 *rec;          // wave-major rating records (+ kRecPad)
+  const int64_t *wblock_ptr; // [p*p + 1]: start of block (b, s) at index b*p + s
+  int64_t *flags;            // [p * kFlagStride]: strata completed by each row-block
+  int32_t *err;              // device error word (0 = ok)
+  int64_t n, m;
+  int32_t k, p;
+  int32_t cols_max;          // largest column-block width
+  int32_t s_begin, s_end;    // strata of this launch
+  int64_t g_base;            // global stratum index of stratum 0 of this epoch
+  int64_t wait_ticks;        // wait limit in s_memrealtime ticks (100 MHz)
+  float alpha, beta;
+  int32_t xcd_remap;
+};
+constexpr int kFlagStride = 16;  // int64 words per flag (one 128-byte line)
+constexpr int kWavesPerGroup = 4;
+constexpr int kErrTimeout = 1;
+constexpr int kErrLayout = 2;  // a bucketing write fell outside its array
+
+// Launchers (defined in the .hip files); all enqueue on `stream`.
+// One wave per row-block; a workgroup holds waves_per_group (1, 2 or 4)
+// row-blocks, each with its own LDS slice of (cols_max + 1) x kp floats.
+hipError_t launch_sgd(const SgdParams &P, int kp, int waves_per_group, bool cooperative,
+                      size_t lds_bytes, hipStream_t stream);
+hipError_t sgd_occupancy(int kp, bool mask, int waves_per_group, size_t lds_bytes,
+                         int *groups_per_cu);
+hipError_t sgd_set_lds_limit(int kp, bool mask, size_t lds_bytes);
+
+hipError_t launch_rmse(const uint2 *rec, const int64_t *wblock_ptr, const float *U,
+                       const float *V, int64_t n, int64_t m, int32_t k, int32_t p, int64_t nnz,
+                       double *partials, double *out, hipStream_t stream);
+size_t rmse_partials_count(int32_t p);
+
+// Bucketing: from device COO to the block layout.  Scratch buffers are
+// allocated by the caller (see bucket_scratch_bytes).
+struct BucketOut {
+  int64_t *block_ptr;   // [p*p + 1] stratum-major slot starts
+  int64_t *wblock_ptr;  // [p*p + 1] wave-major block starts
+  int32_t *perm;        // [nnz] input position of each slot-ordered rating
+  uint2 *rec;           // [nnz + kRecPad] wave-major records
+};
+size_t bucket_scratch_bytes(int64_t nnz, int32_t p);
+hipError_t bucket(const int32_t *rows, const int32_t *cols, const float *vals, int64_t nnz,
+                  int64_t n, int64_t m, int32_t p, bool flag_v_reload, void *scratch,
+                  size_t scratch_bytes, const BucketOut &out, int32_t *err, hipStream_t stream);
+
+}  // namespace bgmfk

@@ -1,0 +1,113 @@
+// Whole-matrix RMSE over the loaded ratings (Algorithm 1's termination
+// test): sqrt((1/nnz) sum (x - u_i.v_j)^2), dot products in fp32, squares
+// summed in fp64.  Reads the wave-major records: workgroup b covers
+// row-block b, its wave w the blocks s = w, w+4, ...; a group of lanes
+// shares one rating and loads 16-byte slices of u_i and v_j.  Per-wave sums
+// are combined in a fixed order by a second kernel, so the result does not
+// depend on scheduling.
+#include "bgmf_internal.h"
+
+namespace bgmfk {
+namespace {
+
+template <int CTRL>
+__device__ __forceinline__ float dpp_mov(float x) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
+}
+
+// KP: padded k; L lanes per rating (4, 8 or 16); each lane covers the
+// float4 slices q = g, g + L, ... of the row.
+template <int KP>
+__global__ void __launch_bounds__(256)
+k_rmse_partial(const uint2 *__restrict__ rec, const int64_t *__restrict__ wblock_ptr,
+               const float *__restrict__ U, const float *__restrict__ V, int64_t n, int64_t m,
+               int32_t k, int32_t p, double *__restrict__ partials) {
+  constexpr int L = KP >= 64 ? 16 : KP / 4;
+  constexpr int RPS = 64 / L;  // ratings per wave step
+  constexpr int Q = KP / 4;    // float4 slices per padded row
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int gl = lane % L, grp = lane / L;
+  const int b = blockIdx.x;
+  const Grid G{n, m, p};
+  const float *Ub = U + G.row_start(b) * k;
+  const uint32_t rmax = (uint32_t)(G.row_start(b + 1) - G.row_start(b)) - 1u;
+  const int kq = k / 4;
+  double acc = 0.0;
+  for (int s = wave; s < p; s += kWavesPerGroup) {
+    const int64_t beg = wblock_ptr[(int64_t)b * p + s];
+    const int64_t end = wblock_ptr[(int64_t)b * p + s + 1];
+    if (beg == end) continue;
+    const int C = (b + s) % p;
+    const float *Vb = V + G.col_start(C) * k;
+    const uint32_t cmax = (uint32_t)(G.col_start(C + 1) - G.col_start(C)) - 1u;
+    for (int64_t t0 = beg; t0 < end; t0 += RPS) {
+      const int64_t t = t0 + grp;
+      const bool ok = t < end;
+      const uint2 r = rec[ok ? t : beg];
+      const uint32_t row = min(r.x & kRowMask, rmax);
+      const uint32_t col = min((r.x >> kColShift) & kColMask, cmax);
+      const float4 *up = reinterpret_cast<const float4 *>(Ub + (int64_t)row * k);
+      const float4 *vp = reinterpret_cast<const float4 *>(Vb + (int64_t)col * k);
+      float part = 0.0f;
+#pragma unroll
+      for (int q = gl; q < Q; q += L) {
+        if (q < kq) {
+          const float4 a = up[q], c = vp[q];
+          part = fmaf(a.x, c.x, part);
+          part = fmaf(a.y, c.y, part);
+          part = fmaf(a.z, c.z, part);
+          part = fmaf(a.w, c.w, part);
+        }
+      }
+      part += dpp_mov<0xB1>(part);
+      if constexpr (L > 2) part += dpp_mov<0x4E>(part);
+      if constexpr (L > 4) part += dpp_mov<0x141>(part);
+      if constexpr (L > 8) part += dpp_mov<0x140>(part);
+      if (ok && gl == 0) {
+        const float d = __uint_as_float(r.y) - part;
+        acc += (double)d * (double)d;
+      }
+    }
+  }
+  for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
+  if (lane == 0) partials[(int64_t)b * kWavesPerGroup + wave] = acc;
+}
+
+__global__ void __launch_bounds__(256)
+k_rmse_final(const double *__restrict__ partials, int64_t count, int64_t nnz, double *out) {
+  __shared__ double sh[256];
+  double a = 0.0;
+  for (int64_t i = threadIdx.x; i < count; i += 256) a += partials[i];
+  sh[threadIdx.x] = a;
+  __syncthreads();
+  for (int off = 128; off > 0; off >>= 1) {
+    if ((int)threadIdx.x < off) sh[threadIdx.x] += sh[threadIdx.x + off];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) out[0] = nnz > 0 ? sqrt(sh[0] / (double)nnz) : 0.0;
+}
+
+}  // namespace
+
+size_t rmse_partials_count(int32_t p) { return (size_t)p * kWavesPerGroup; }
+
+hipError_t launch_rmse(const uint2 *rec, const int64_t *wblock_ptr, const float *U,
+                       const float *V, int64_t n, int64_t m, int32_t k, int32_t p, int64_t nnz,
+                       double *partials, double *out, hipStream_t stream) {
+  int kp = 16;
+  while (kp < k) kp <<= 1;
+  const dim3 grid((unsigned)p), block(256);
+  switch (kp) {
+    case 16: hipLaunchKernelGGL(k_rmse_partial<16>, grid, block, 0, stream, rec, wblock_ptr, U, V, n, m, k, p, partials); break;
+    case 32: hipLaunchKernelGGL(k_rmse_partial<32>, grid, block, 0, stream, rec, wblock_ptr, U, V, n, m, k, p, partials); break;
+    case 64: hipLaunchKernelGGL(k_rmse_partial<64>, grid, block, 0, stream, rec, wblock_ptr, U, V, n, m, k, p, partials); break;
+    case 128: hipLaunchKernelGGL(k_rmse_partial<128>, grid, block, 0, stream, rec, wblock_ptr, U, V, n, m, k, p, partials); break;
+    case 256: hipLaunchKernelGGL(k_rmse_partial<256>, grid, block, 0, stream, rec, wblock_ptr, U, V, n, m, k, p, partials); break;
+    default: return hipErrorInvalidValue;
+  }
+  hipLaunchKernelGGL(k_rmse_final, dim3(1), dim3(256), 0, stream, partials,
+                     (int64_t)rmse_partials_count(p), nnz, out);
+  return hipGetLastError();
+}
+
+}  // namespace bgmfk
