@@ -72,22 +72,26 @@ def cpu_baseline(w, budget_s):
         used = oracle.epoch_mt(p, w.rows, w.cols, w.vals, sub, perm, U, V, w.alpha, w.beta, threads)
         return time.perf_counter() - t, int(bp[hi] - bp[lo]), used
 
-    # calibrate on a few strata, then size the sample
-    c = max(1, min(8, p // 8))
-    dt, cnt, used = run_strata(0, c)
-    rate = cnt / max(dt, 1e-9)
-    per_stratum = max(1, w.nnz // p)
-    n_strata = int(max(1, min(p - c, budget_s * rate / per_stratum)))
-    dt, cnt, used = run_strata(c, c + n_strata)
+    # run strata in order (wrapping into further epochs) until the time
+    # budget is used up
+    s0, done, spent, used = 0, 0, 0.0, threads
+    chunk = max(1, min(p, 16))
+    while spent < budget_s:
+        s1 = min(p, s0 + chunk)
+        dt, cnt, used = run_strata(s0, s1)
+        spent += dt
+        done += cnt
+        s0 = 0 if s1 == p else s1
+    dt, cnt = spent, done
     return {
         "value": cnt / dt,
         "unit": "updates/s",
         "cores": used,
         "kind": "oracle",
         "sample": (f"oracle blocked epoch (C, fp32, {used} threads splitting each stratum's "
-                   f"blocks) over strata {c}..{c + n_strata - 1} of {p} of the same workload: {cnt} "
-                   f"rating updates in {dt:.2f} s; oracle bucketing of all {w.nnz} ratings "
-                   f"took {t_bucket:.1f} s (untimed)"),
+                   f"blocks, strata in order from stratum 0) on the same workload: {cnt} rating "
+                   f"updates in {dt:.2f} s; oracle bucketing of all {w.nnz} ratings took "
+                   f"{t_bucket:.1f} s (untimed)"),
     }
 
 

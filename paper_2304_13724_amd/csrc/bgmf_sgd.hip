@@ -34,28 +34,6 @@ __device__ __forceinline__ float dpp_mov(float x) {
   return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
 }
 
-// Sum over the lanes holding dimensions (all 64 for KP >= 64); every lane
-// returns the same bits (each step adds two values whose sum is commutative).
-template <int KP>
-__device__ __forceinline__ float lane_sum(float x) {
-#pragma clang fp contract(off)
-  x = x + dpp_mov<0xB1>(x);   // quad_perm [1,0,3,2]
-  x = x + dpp_mov<0x4E>(x);   // quad_perm [2,3,0,1]
-  if constexpr (KP > 4) x = x + dpp_mov<0x141>(x);  // row_half_mirror
-  if constexpr (KP > 8) x = x + dpp_mov<0x140>(x);  // row_mirror
-  if constexpr (KP > 16) {
-    auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false,
-                                              false);
-    x = __uint_as_float(r[0]) + __uint_as_float(r[1]);
-  }
-  if constexpr (KP > 32) {
-    auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
-                                              false);
-    x = __uint_as_float(r[0]) + __uint_as_float(r[1]);
-  }
-  return x;
-}
-
 __device__ __forceinline__ uint32_t rl(uint32_t v, int lane) {
   return (uint32_t)__builtin_amdgcn_readlane((int)v, lane);
 }
@@ -66,7 +44,39 @@ __device__ __forceinline__ int64_t uniform64(int64_t x) {
   return (int64_t)(((uint64_t)hi << 32) | lo);
 }
 
-// Wait until *flag >= target, then acquire.  Returns false on timeout.
+// Hand-over of a column slice between neighbouring waves.
+//
+// The slice is written back with device-scope (sc1) stores and staged in
+// with device-scope (sc1) loads, both coherent across the XCDs' L2 caches.
+// The writer waits for its stores to complete (vmcnt(0), the release fence
+// at workgroup scope) before it stores its progress word; the reader waits
+// for the progress word (and for that load to return) before it issues the
+// loads of the slice, and a workgroup-scope acquire fence keeps the compiler
+// from moving them earlier.  An agent-scope release/acquire fence would add
+// a write-back / invalidation of the whole L2 of the XCD; it is only needed
+// to publish or refresh plain cached accesses, and the hand-over uses none.
+constexpr int kCoherent = 16;  // cache-policy bits of a device-scope access (sc1)
+
+// Buffer descriptor word 3 for gfx9 (32-bit data format); accesses whose
+// VGPR offset is at or past num_records return 0 / are dropped.
+constexpr int kBufWord3 = 0x00020000;
+constexpr uint32_t kOff = 0x40000000u;  // outside every buffer, even when added twice
+
+__device__ __forceinline__ float buf_ld(__amdgpu_buffer_rsrc_t r, uint32_t voff) {
+  return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, (int)voff, 0, 0));
+}
+__device__ __forceinline__ void buf_st(float x, __amdgpu_buffer_rsrc_t r, uint32_t voff) {
+  __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(x), r, (int)voff, 0, 0);
+}
+
+__device__ __forceinline__ float buf_ld_coherent(__amdgpu_buffer_rsrc_t r, uint32_t voff) {
+  return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, (int)voff, 0, kCoherent));
+}
+__device__ __forceinline__ void buf_st_coherent(float x, __amdgpu_buffer_rsrc_t r, uint32_t voff) {
+  __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(x), r, (int)voff, 0, kCoherent);
+}
+
+// Wait until *flag >= target.  Returns false on timeout.
 __device__ __forceinline__ bool wait_progress(const int64_t *flag, int64_t target,
                                               int64_t wait_ticks) {
   if (__hip_atomic_load(flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
@@ -76,8 +86,46 @@ __device__ __forceinline__ bool wait_progress(const int64_t *flag, int64_t targe
       if ((int64_t)(__builtin_amdgcn_s_memrealtime() - t0) > wait_ticks) return false;
     }
   }
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
   return true;
+}
+
+// Publish progress: all earlier stores of the wave (the column slice) have
+// completed before the progress word is written.
+__device__ __forceinline__ void publish_progress(int64_t *flag, int64_t value) {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __hip_atomic_store(flag, value, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// In-row sum (16 lanes) leaving the row's total in every lane of the row.
+__device__ __forceinline__ float row_sum(float x) {
+#pragma clang fp contract(off)
+  x = x + dpp_mov<0xB1>(x);   // quad_perm [1,0,3,2]
+  x = x + dpp_mov<0x4E>(x);   // quad_perm [2,3,0,1]
+  x = x + dpp_mov<0x141>(x);  // row_half_mirror
+  x = x + dpp_mov<0x140>(x);  // row_mirror
+  return x;
+}
+
+// Sum over the lanes that hold distinct dimensions, returned as a scalar
+// (the value of lane 63).  KPL = lanes holding one copy (16, 32 or 64).
+// The two broadcast steps are written as single DPP adds with a row mask
+// (rows outside the mask keep their value); each is preceded by the two
+// wait states a DPP read of a just-written VGPR needs.
+template <int KPL>
+__device__ __forceinline__ float lane_total(float x) {
+  x = row_sum(x);
+  if constexpr (KPL >= 32)  // rows 1 and 3 add the last lane of rows 0 and 2
+    asm("s_nop 1\n\tv_add_f32_dpp %0, %0, %0 row_bcast:15 row_mask:0xa bank_mask:0xf"
+        : "+v"(x));
+  if constexpr (KPL >= 64)  // rows 2 and 3 add lane 31; lane 63 then holds the total
+    asm("s_nop 1\n\tv_add_f32_dpp %0, %0, %0 row_bcast:31 row_mask:0xc bank_mask:0xf"
+        : "+v"(x));
+  return __uint_as_float((uint32_t)__builtin_amdgcn_readlane(__float_as_int(x), 63));
+}
+
+__device__ __forceinline__ float &lds_at(char *base, uint32_t byte_off) {
+  return *reinterpret_cast<float *>(base + byte_off);
 }
 
 // KP: k rounded up to a power of two (>= 16).  Lane l holds dimensions
@@ -85,9 +133,13 @@ __device__ __forceinline__ bool wait_progress(const int64_t *flag, int64_t targe
 // KP < 64 (then the 64/KP lane groups hold identical copies, compute the
 // same values and store them to the same addresses).  MASK: k < KP, so the
 // dimensions >= k are padding (kept at zero, never stored).
+//
+// Error term: every lane adds x/KPL to its partial products, so the lane
+// total is e = x - u.v directly (x/KPL is an exact power-of-two scaling).
 template <int KP, bool MASK>
 __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
   constexpr int NV = KP <= 64 ? 1 : KP / 64;
+  constexpr int KPL = KP < 64 ? KP : 64;
   constexpr int D = kPrefetch;
   constexpr int CH = D;  // ratings per unrolled chunk; ring slot = step in chunk
   const int lane = threadIdx.x & 63;
@@ -105,22 +157,32 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
   if (b >= P.p) return;
 
   extern __shared__ float lds[];
-  // per wave: cols_max + 1 column slots; the last one absorbs padding steps
-  float *vblk = lds + (size_t)wave * (P.cols_max + 1) * KP + dim;
   const Grid G{P.n, P.m, P.p};
   const int k = P.k;
+  const uint32_t rowbytes = (uint32_t)k * 4u;
+  const uint32_t colbytes = (uint32_t)KP * 4u;
   bool act[NV];
 #pragma unroll
   for (int v = 0; v < NV; ++v) act[v] = !MASK || (dim + 64 * v < k);
-  float *Ub = P.U + G.row_start(b) * k + dim;
-  // local rows are < rmax + 1 by construction; the clamps below keep every
-  // address inside U even if a record were corrupt
-  const uint32_t rmax = (uint32_t)(G.row_start(b + 1) - G.row_start(b)) - 1u;
-  float *Udummy = P.U + P.n * (int64_t)k + dim;  // one spare row after U
+  // byte offset of this lane's dimension v inside a row; padding
+  // dimensions get an out-of-range offset (loads 0, stores dropped)
+  uint32_t doff[NV];
+#pragma unroll
+  for (int v = 0; v < NV; ++v) doff[v] = act[v] ? (uint32_t)(dim + 64 * v) * 4u : kOff;
+
+  // U rows of row-block b (owned by this wave for the whole launch)
+  const int64_t r0 = G.row_start(b);
+  const uint32_t rows_b = (uint32_t)(G.row_start(b + 1) - r0);
+  const __amdgpu_buffer_rsrc_t Ures =
+      __builtin_amdgcn_make_buffer_rsrc(P.U + r0 * k, (short)0, (int)(rows_b * rowbytes), kBufWord3);
+  // this wave's LDS column slots: cols_max real ones and one spare
+  const uint32_t vbase = ((uint32_t)wave * (P.cols_max + 1) * KP + dim) * 4u;
+  const uint32_t spare = (uint32_t)P.cols_max * colbytes;
+  char *ldsb = reinterpret_cast<char *>(lds);
   const int64_t *wbp = P.wblock_ptr + (int64_t)b * P.p;
-  const float alpha = P.alpha, nbeta = -P.beta;
-  const uint32_t cmax = (uint32_t)P.cols_max - 1u;
-  const uint32_t cdummy = (uint32_t)P.cols_max;
+  const float alpha = P.alpha;
+  const float shrink = 1.0f - P.alpha * P.beta;  // u + a(e v - b u) = (1 - a b) u + (a e) v
+  const float xscale = 1.0f / (float)KPL;
 
   for (int s = P.s_begin; s < P.s_end; ++s) {
     const int64_t g = P.g_base + s;
@@ -131,17 +193,30 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
     const int32_t len = (int32_t)(uniform64(wbp[s + 1]) - beg);
     const uint2 *rp = P.rec + beg;
 
+    // Decoded window of 64 records starting at chunk position c:
+    //   wrow = byte offset of the row in U (kOff past the block end)
+    //   wcol = byte offset of the column slot in LDS (spare past the end)
+    //   wx   = x / KPL
+    uint32_t wrow = kOff, wcol = spare;
+    float wx = 0.0f;
+    auto decode = [&](uint2 w, int32_t c) {
+      const bool ok = c + lane < len;
+      wrow = ok ? (w.x & kRowMask) * rowbytes : kOff;
+      wcol = ok ? ((w.x >> kColShift) & kColMask) * colbytes : spare;
+      wx = __uint_as_float(w.y) * xscale;
+    };
+
     // ratings of the block and the u rows of its first D ratings: these do
     // not depend on V, so they are requested before the wait
-    uint2 W = make_uint2(0u, 0u);
     float ring[D][NV];
+    uint32_t ringrow[D];
     if (len > 0) {
-      W = rp[lane];
+      decode(rp[lane], 0);
 #pragma unroll
       for (int j = 0; j < D; ++j) {
-        const uint32_t row = (j < len) ? min(rl(W.x, j) & kRowMask, rmax) : 0u;
+        ringrow[j] = rl(wrow, j);
 #pragma unroll
-        for (int v = 0; v < NV; ++v) ring[j][v] = act[v] ? Ub[row * k + 64 * v] : 0.0f;
+        for (int v = 0; v < NV; ++v) ring[j][v] = buf_ld(Ures, doff[v] + ringrow[j]);
       }
     }
     if (s > P.s_begin) {
@@ -153,19 +228,28 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
       }
     }
     if (len > 0) {
-      const float *Vc = P.V + c0 * k + dim;
-      for (int c = 0; c < ncols; ++c) {
+      // stage the column slice of V in LDS, 16 columns per round trip
+      const __amdgpu_buffer_rsrc_t Vres = __builtin_amdgcn_make_buffer_rsrc(
+          P.V + c0 * k, (short)0, (int)((uint32_t)ncols * rowbytes), kBufWord3);
+      for (int cb = 0; cb < ncols; cb += 16) {
+        float tmp[16][NV];
 #pragma unroll
-        for (int v = 0; v < NV; ++v)
-          vblk[c * KP + 64 * v] = act[v] ? Vc[(int64_t)c * k + 64 * v] : 0.0f;
+        for (int i = 0; i < 16; ++i)
+#pragma unroll
+          for (int v = 0; v < NV; ++v)
+            tmp[i][v] = buf_ld_coherent(Vres, doff[v] + (uint32_t)(cb + i) * rowbytes);
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const uint32_t slot = (uint32_t)min(cb + i, P.cols_max);
+#pragma unroll
+          for (int v = 0; v < NV; ++v)
+            lds_at(ldsb, vbase + slot * colbytes + 256u * v) = tmp[i][v];
+        }
       }
-      uint32_t meta = rl(W.x, 0);
+      uint32_t waddr = vbase + rl(wcol, 0);  // LDS address of the current column
       float vnext[NV];
-      {
-        const uint32_t cf = min((meta >> kColShift) & kColMask, cmax);
 #pragma unroll
-        for (int v = 0; v < NV; ++v) vnext[v] = vblk[cf * KP + 64 * v];
-      }
+      for (int v = 0; v < NV; ++v) vnext[v] = lds_at(ldsb, waddr + 256u * v);
       uint32_t prev_row = 0xFFFFFFFFu;
       float uprev[NV];
 #pragma unroll
@@ -176,15 +260,14 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
       __builtin_amdgcn_s_waitcnt(0x0F70);
 
       for (int32_t c = 0; c < len; c += CH) {
-        // records c .. c+63 are in W; fetch the next window now
+        // records c .. c+63 are decoded; fetch the next window now
         const uint2 Wn = rp[c + CH + lane];
+        uint32_t ccur = rl(wcol, 0);
 #pragma unroll
         for (int j = 0; j < CH; ++j) {
-          const int32_t t = c + j;
-          const bool valid = t < len;  // steps past the end update spare slots
-          const float x = __uint_as_float(rl(W.y, j));
-          const uint32_t row = min(meta & kRowMask, rmax);
-          const uint32_t col = valid ? min((meta >> kColShift) & kColMask, cmax) : cdummy;
+          const float x64 = __uint_as_float(rl(__float_as_uint(wx), j));
+          const uint32_t row = ringrow[j];
+          const uint32_t col1 = rl(wcol, j + 1);
           const bool same_row = row == prev_row;
           float u[NV], vv[NV];
 #pragma unroll
@@ -194,50 +277,57 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
           }
           // read v of the next rating now; if it is the same column the
           // value computed below is forwarded instead
-          const uint32_t meta1 = rl(W.x, j + 1);
-          const uint32_t col1 = min((meta1 >> kColShift) & kColMask, cmax);
+          const uint32_t raddr = vbase + col1;
           float vl[NV];
 #pragma unroll
-          for (int v = 0; v < NV; ++v) vl[v] = vblk[col1 * KP + 64 * v];
+          for (int v = 0; v < NV; ++v) vl[v] = lds_at(ldsb, raddr + 256u * v);
 
-          float pr = u[0] * vv[0];
+          float tpart = fmaf(-u[0], vv[0], x64);
 #pragma unroll
-          for (int v = 1; v < NV; ++v) pr = fmaf(u[v], vv[v], pr);
-          const float e = x - lane_sum<KP>(pr);
+          for (int v = 1; v < NV; ++v) tpart = fmaf(-u[v], vv[v], tpart);
+          const float ae = alpha * lane_total<KPL>(tpart);
           float nu[NV], nv[NV];
 #pragma unroll
           for (int v = 0; v < NV; ++v) {
-            nu[v] = fmaf(alpha, fmaf(e, vv[v], nbeta * u[v]), u[v]);
-            nv[v] = fmaf(alpha, fmaf(e, u[v], nbeta * vv[v]), vv[v]);
+            nu[v] = fmaf(ae, vv[v], shrink * u[v]);
+            nv[v] = fmaf(ae, u[v], shrink * vv[v]);
           }
-          float *ud = valid ? Ub + row * k : Udummy;
 #pragma unroll
           for (int v = 0; v < NV; ++v) {
-            vblk[col * KP + 64 * v] = nv[v];
-            if (act[v]) ud[64 * v] = nu[v];
+            lds_at(ldsb, waddr + 256u * v) = nv[v];
+            buf_st(nu[v], Ures, doff[v] + row);
             uprev[v] = nu[v];
-            vnext[v] = (col1 == col) ? nv[v] : vl[v];
+            vnext[v] = (col1 == ccur) ? nv[v] : vl[v];
           }
           prev_row = row;
-          meta = meta1;
+          ccur = col1;
+          waddr = raddr;
           // prefetch the u row of rating t + D into the slot just freed
-          const uint32_t rowD = min(rl(W.x, j + D) & kRowMask, rmax) & (t + D < len ? kRowMask : 0u);
+          ringrow[j] = rl(wrow, j + D);
 #pragma unroll
-          for (int v = 0; v < NV; ++v) ring[j][v] = act[v] ? Ub[rowD * k + 64 * v] : 0.0f;
+          for (int v = 0; v < NV; ++v) ring[j][v] = buf_ld(Ures, doff[v] + ringrow[j]);
         }
-        W = Wn;
+        decode(Wn, c + CH);
       }
-      // publish the column slice
-      float *Vw = P.V + c0 * k + dim;
-      for (int c = 0; c < ncols; ++c) {
+      // publish the column slice, 16 columns per round
+      for (int cb = 0; cb < ncols; cb += 16) {
+        float tmp[16][NV];
 #pragma unroll
-        for (int v = 0; v < NV; ++v)
-          if (act[v]) Vw[(int64_t)c * k + 64 * v] = vblk[c * KP + 64 * v];
+        for (int i = 0; i < 16; ++i) {
+          const uint32_t slot = (uint32_t)min(cb + i, P.cols_max);
+#pragma unroll
+          for (int v = 0; v < NV; ++v) tmp[i][v] = lds_at(ldsb, vbase + slot * colbytes + 256u * v);
+        }
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+#pragma unroll
+          for (int v = 0; v < NV; ++v)
+            buf_st_coherent(tmp[i][v], Vres, doff[v] + (uint32_t)(cb + i) * rowbytes);
       }
     }
-    // every lane releases its own stores (all write the same value)
-    __hip_atomic_store(P.flags + (int64_t)b * kFlagStride, g + 1, __ATOMIC_RELEASE,
-                       __HIP_MEMORY_SCOPE_AGENT);
+    // a launch of one stratum is ordered by the kernel boundary instead;
+    // every lane publishes its own stores (all write the same value)
+    if (P.s_end - P.s_begin > 1) publish_progress(P.flags + (int64_t)b * kFlagStride, g + 1);
   }
 }
 

@@ -179,3 +179,19 @@ def test_wait_limit_error_path():
         U, V = mdl.get_factors()
     U_ref, V_ref, _, _, _ = oracle_run(w, 1)
     assert row_rel_err(U, U_ref) <= TOL and row_rel_err(V, V_ref) <= TOL
+
+
+@pytest.mark.parametrize("k,p", [(64, 512), (16, 1024), (128, 256)])
+def test_handover_stress(k, p):
+    """Many strata with few ratings per block: every epoch is mostly
+    column-slice hand-overs between neighbouring waves.  Three epochs must
+    match the oracle and repeat bit for bit."""
+    w = make("hs", n=4 * p + 37, m=2 * p + 11, nnz=40 * p, k=k, p=p, alpha=0.02, beta=0.05,
+             epochs=3, seed=p + k, structure="uniform", values="int5", rank=4)
+    U_ref, V_ref, hist_ref, _, _ = oracle_run(w, 3)
+    a = gpu_run(w, 3)
+    b = gpu_run(w, 3)
+    assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
+    assert row_rel_err(a[0], U_ref) <= TOL and row_rel_err(a[1], V_ref) <= TOL
+    for x, y in zip(a[2], hist_ref):
+        assert abs(x - y) <= TOL * y
