@@ -22,9 +22,11 @@ __global__ void __launch_bounds__(256)
 k_rmse_partial(const uint2 *__restrict__ rec, const int64_t *__restrict__ wblock_ptr,
                const float *__restrict__ U, const float *__restrict__ V, int64_t n, int64_t m,
                int32_t k, int32_t p, double *__restrict__ partials) {
-  constexpr int L = KP >= 64 ? 16 : KP / 4;
-  constexpr int RPS = 64 / L;  // ratings per wave step
-  constexpr int Q = KP / 4;    // float4 slices per padded row
+  constexpr int L = KP >= 64 ? 16 : KP / 4;  // lanes per rating
+  constexpr int RPS = 64 / L;                // ratings per wave step
+  constexpr int Q = KP / 4;                  // float4 slices per padded row
+  constexpr int QL = (Q + L - 1) / L;        // slices per lane
+  constexpr int UNR = 4;                     // wave steps whose loads are in flight together
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int gl = lane % L, grp = lane / L;
   const int b = blockIdx.x;
@@ -40,32 +42,46 @@ k_rmse_partial(const uint2 *__restrict__ rec, const int64_t *__restrict__ wblock
     const int C = (b + s) % p;
     const float *Vb = V + G.col_start(C) * k;
     const uint32_t cmax = (uint32_t)(G.col_start(C + 1) - G.col_start(C)) - 1u;
-    for (int64_t t0 = beg; t0 < end; t0 += RPS) {
-      const int64_t t = t0 + grp;
-      const bool ok = t < end;
-      const uint2 r = rec[ok ? t : beg];
-      const uint32_t row = min(r.x & kRowMask, rmax);
-      const uint32_t col = min((r.x >> kColShift) & kColMask, cmax);
-      const float4 *up = reinterpret_cast<const float4 *>(Ub + (int64_t)row * k);
-      const float4 *vp = reinterpret_cast<const float4 *>(Vb + (int64_t)col * k);
-      float part = 0.0f;
+    for (int64_t t0 = beg; t0 < end; t0 += RPS * UNR) {
+      float4 a[UNR][QL], c[UNR][QL];
+      float x[UNR];
+      bool ok[UNR];
 #pragma unroll
-      for (int q = gl; q < Q; q += L) {
-        if (q < kq) {
-          const float4 a = up[q], c = vp[q];
-          part = fmaf(a.x, c.x, part);
-          part = fmaf(a.y, c.y, part);
-          part = fmaf(a.z, c.z, part);
-          part = fmaf(a.w, c.w, part);
+      for (int u = 0; u < UNR; ++u) {
+        const int64_t t = t0 + u * RPS + grp;
+        ok[u] = t < end;
+        const uint2 r = rec[ok[u] ? t : beg];
+        x[u] = __uint_as_float(r.y);
+        const uint32_t row = min(r.x & kRowMask, rmax);
+        const uint32_t col = min((r.x >> kColShift) & kColMask, cmax);
+        const float4 *up = reinterpret_cast<const float4 *>(Ub + (int64_t)row * k);
+        const float4 *vp = reinterpret_cast<const float4 *>(Vb + (int64_t)col * k);
+#pragma unroll
+        for (int i = 0; i < QL; ++i) {
+          const int q = gl + i * L;
+          const bool in = q < kq;
+          a[u][i] = in ? up[q] : make_float4(0.f, 0.f, 0.f, 0.f);
+          c[u][i] = in ? vp[q] : make_float4(0.f, 0.f, 0.f, 0.f);
         }
       }
-      part += dpp_mov<0xB1>(part);
-      if constexpr (L > 2) part += dpp_mov<0x4E>(part);
-      if constexpr (L > 4) part += dpp_mov<0x141>(part);
-      if constexpr (L > 8) part += dpp_mov<0x140>(part);
-      if (ok && gl == 0) {
-        const float d = __uint_as_float(r.y) - part;
-        acc += (double)d * (double)d;
+#pragma unroll
+      for (int u = 0; u < UNR; ++u) {
+        float part = 0.0f;
+#pragma unroll
+        for (int i = 0; i < QL; ++i) {
+          part = fmaf(a[u][i].x, c[u][i].x, part);
+          part = fmaf(a[u][i].y, c[u][i].y, part);
+          part = fmaf(a[u][i].z, c[u][i].z, part);
+          part = fmaf(a[u][i].w, c[u][i].w, part);
+        }
+        part += dpp_mov<0xB1>(part);
+        if constexpr (L > 2) part += dpp_mov<0x4E>(part);
+        if constexpr (L > 4) part += dpp_mov<0x141>(part);
+        if constexpr (L > 8) part += dpp_mov<0x140>(part);
+        if (ok[u] && gl == 0) {
+          const float d = x[u] - part;
+          acc += (double)d * (double)d;
+        }
       }
     }
   }
