@@ -412,7 +412,7 @@ int bgmf_rmse(bgmf_t *h, double *out) {
   if (!h->factors_set) return fail(h, BGMF_E_STATE, "bgmf_rmse: factors not set");
   HIP_TRY(h, hipEventRecord(h->ev[2], h->stream));
   HIP_TRY(h, launch_rmse(h->rec, h->wblock_ptr, h->U, h->V, h->n, h->m, h->k, h->p, h->nnz,
-                         h->partials, h->d_rmse, h->stream));
+                         h->partials, h->d_rmse, h->lds_limit, h->stream));
   HIP_TRY(h, hipEventRecord(h->ev[3], h->stream));
   h->rmse_timed = true;
   double r = 0.0;

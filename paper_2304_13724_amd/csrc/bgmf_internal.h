@@ -18,7 +18,10 @@ constexpr int kColBits = 14;
 constexpr uint32_t kRowMask = (1u << kRowBits) - 1u;
 constexpr uint32_t kColMask = (1u << kColBits) - 1u;
 constexpr uint32_t kFlagVReload = 1u << 30;  // v_j was updated 2..kPrefetch-1 ratings ago
-constexpr int kPrefetch = 16;                // prefetch distance of factor rows (ratings)
+#ifndef BGMF_PREFETCH
+#define BGMF_PREFETCH 16
+#endif
+constexpr int kPrefetch = BGMF_PREFETCH;     // prefetch distance of factor rows (ratings)
 constexpr int kRecPad = 256;                 // padding records after the last stream
 
 // Block geometry of the p x p grid: row-block R holds rows
@@ -67,7 +70,7 @@ hipError_t sgd_set_lds_limit(int kp, bool mask, size_t lds_bytes);
 
 hipError_t launch_rmse(const uint2 *rec, const int64_t *wblock_ptr, const float *U,
                        const float *V, int64_t n, int64_t m, int32_t k, int32_t p, int64_t nnz,
-                       double *partials, double *out, hipStream_t stream);
+                       double *partials, double *out, size_t lds_limit, hipStream_t stream);
 size_t rmse_partials_count(int32_t p);
 
 // Bucketing: from device COO to the block layout.  Scratch buffers are

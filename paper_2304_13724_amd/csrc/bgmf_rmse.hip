@@ -5,10 +5,14 @@
 // shares one rating and loads 16-byte slices of u_i and v_j.  Per-wave sums
 // are combined in a fixed order by a second kernel, so the result does not
 // depend on scheduling.
+#include <algorithm>
+
 #include "bgmf_internal.h"
 
 namespace bgmfk {
 namespace {
+
+constexpr int kRmseSplit = 4;  // workgroups per row-block (each takes a quarter of its strata)
 
 template <int CTRL>
 __device__ __forceinline__ float dpp_mov(float x) {
@@ -26,42 +30,60 @@ k_rmse_partial(const uint2 *__restrict__ rec, const int64_t *__restrict__ wblock
   constexpr int RPS = 64 / L;                // ratings per wave step
   constexpr int Q = KP / 4;                  // float4 slices per padded row
   constexpr int QL = (Q + L - 1) / L;        // slices per lane
-  constexpr int UNR = 4;                     // wave steps whose loads are in flight together
+  constexpr int UNR = 8;                     // wave steps whose loads are in flight together
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int gl = lane % L, grp = lane / L;
-  const int b = blockIdx.x;
+  const int b = blockIdx.x / kRmseSplit;          // row-block
+  const int w0 = (blockIdx.x % kRmseSplit) * kWavesPerGroup + wave;  // first stratum
   const Grid G{n, m, p};
   const float *Ub = U + G.row_start(b) * k;
   const uint32_t rmax = (uint32_t)(G.row_start(b + 1) - G.row_start(b)) - 1u;
   const int kq = k / 4;
   double acc = 0.0;
-  for (int s = wave; s < p; s += kWavesPerGroup) {
+  for (int s = w0; s < p; s += kWavesPerGroup * kRmseSplit) {
     const int64_t beg = wblock_ptr[(int64_t)b * p + s];
     const int64_t end = wblock_ptr[(int64_t)b * p + s + 1];
     if (beg == end) continue;
     const int C = (b + s) % p;
     const float *Vb = V + G.col_start(C) * k;
     const uint32_t cmax = (uint32_t)(G.col_start(C + 1) - G.col_start(C)) - 1u;
+    // records of the next iteration are loaded one iteration ahead, so the
+    // factor-row loads never wait for a record load
+    uint2 rn[UNR];
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) {
+      const int64_t t = beg + u * RPS + grp;
+      rn[u] = rec[t < end ? t : beg];
+    }
     for (int64_t t0 = beg; t0 < end; t0 += RPS * UNR) {
       float4 a[UNR][QL], c[UNR][QL];
       float x[UNR];
       bool ok[UNR];
+      uint2 r[UNR];
+#pragma unroll
+      for (int u = 0; u < UNR; ++u) {
+        r[u] = rn[u];
+        const int64_t t = t0 + RPS * UNR + u * RPS + grp;
+        rn[u] = rec[t < end ? t : beg];
+      }
 #pragma unroll
       for (int u = 0; u < UNR; ++u) {
         const int64_t t = t0 + u * RPS + grp;
         ok[u] = t < end;
-        const uint2 r = rec[ok[u] ? t : beg];
-        x[u] = __uint_as_float(r.y);
-        const uint32_t row = min(r.x & kRowMask, rmax);
-        const uint32_t col = min((r.x >> kColShift) & kColMask, cmax);
+        x[u] = __uint_as_float(r[u].y);
+        const uint32_t row = min(r[u].x & kRowMask, rmax);
+        const uint32_t col = min((r[u].x >> kColShift) & kColMask, cmax);
         const float4 *up = reinterpret_cast<const float4 *>(Ub + (int64_t)row * k);
         const float4 *vp = reinterpret_cast<const float4 *>(Vb + (int64_t)col * k);
 #pragma unroll
         for (int i = 0; i < QL; ++i) {
+          // branch-free: slices past k read slice 0 and are zeroed after
           const int q = gl + i * L;
           const bool in = q < kq;
-          a[u][i] = in ? up[q] : make_float4(0.f, 0.f, 0.f, 0.f);
-          c[u][i] = in ? vp[q] : make_float4(0.f, 0.f, 0.f, 0.f);
+          const int qc = in ? q : 0;
+          a[u][i] = up[qc];
+          c[u][i] = vp[qc];
+          if (!in) a[u][i] = make_float4(0.f, 0.f, 0.f, 0.f);
         }
       }
 #pragma unroll
@@ -78,15 +100,110 @@ k_rmse_partial(const uint2 *__restrict__ rec, const int64_t *__restrict__ wblock
         if constexpr (L > 2) part += dpp_mov<0x4E>(part);
         if constexpr (L > 4) part += dpp_mov<0x141>(part);
         if constexpr (L > 8) part += dpp_mov<0x140>(part);
-        if (ok[u] && gl == 0) {
-          const float d = x[u] - part;
-          acc += (double)d * (double)d;
-        }
+        const float d = (ok[u] && gl == 0) ? x[u] - part : 0.0f;
+        acc = fma((double)d, (double)d, acc);
       }
     }
   }
   for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
-  if (lane == 0) partials[(int64_t)b * kWavesPerGroup + wave] = acc;
+  if (lane == 0) partials[(int64_t)blockIdx.x * kWavesPerGroup + wave] = acc;
+}
+
+// Variant with the row-block's U rows staged in LDS: one workgroup of 16
+// waves per row-block, u_i read from LDS, v_j from global memory (L2).
+// Used when rows x k x 4 bytes fit in LDS.
+constexpr int kLdsWaves = 16;
+
+template <int KP>
+__global__ void __launch_bounds__(1024)
+k_rmse_lds(const uint2 *__restrict__ rec, const int64_t *__restrict__ wblock_ptr,
+           const float *__restrict__ U, const float *__restrict__ V, int64_t n, int64_t m,
+           int32_t k, int32_t p, double *__restrict__ partials) {
+  constexpr int L = KP >= 64 ? 16 : KP / 4;
+  constexpr int RPS = 64 / L;
+  constexpr int Q = KP / 4;
+  constexpr int QL = (Q + L - 1) / L;
+  constexpr int UNR = 8;
+  extern __shared__ float4 us[];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int gl = lane % L, grp = lane / L;
+  const int b = blockIdx.x;
+  const Grid G{n, m, p};
+  const int64_t r0 = G.row_start(b);
+  const uint32_t rows_b = (uint32_t)(G.row_start(b + 1) - r0);
+  const uint32_t rmax = rows_b - 1u;
+  const int kq = k / 4;
+  {  // the row-block's rows are contiguous in U
+    const float4 *src = reinterpret_cast<const float4 *>(U + r0 * k);
+    const uint32_t total = rows_b * (uint32_t)kq;
+    for (uint32_t i = threadIdx.x; i < total; i += blockDim.x) us[i] = src[i];
+  }
+  __syncthreads();
+  double acc = 0.0;
+  for (int s = wave; s < p; s += kLdsWaves) {
+    const int64_t beg = wblock_ptr[(int64_t)b * p + s];
+    const int64_t end = wblock_ptr[(int64_t)b * p + s + 1];
+    if (beg == end) continue;
+    const int C = (b + s) % p;
+    const float *Vb = V + G.col_start(C) * k;
+    const uint32_t cmax = (uint32_t)(G.col_start(C + 1) - G.col_start(C)) - 1u;
+    uint2 rn[UNR];
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) {
+      const int64_t t = beg + u * RPS + grp;
+      rn[u] = rec[t < end ? t : beg];
+    }
+    for (int64_t t0 = beg; t0 < end; t0 += RPS * UNR) {
+      float4 a[UNR][QL], c[UNR][QL];
+      float x[UNR];
+      bool ok[UNR];
+      uint2 r[UNR];
+#pragma unroll
+      for (int u = 0; u < UNR; ++u) {
+        r[u] = rn[u];
+        const int64_t t = t0 + RPS * UNR + u * RPS + grp;
+        rn[u] = rec[t < end ? t : beg];
+      }
+#pragma unroll
+      for (int u = 0; u < UNR; ++u) {
+        const int64_t t = t0 + u * RPS + grp;
+        ok[u] = t < end;
+        x[u] = __uint_as_float(r[u].y);
+        const uint32_t row = min(r[u].x & kRowMask, rmax);
+        const uint32_t col = min((r[u].x >> kColShift) & kColMask, cmax);
+        const float4 *vp = reinterpret_cast<const float4 *>(Vb + (int64_t)col * k);
+#pragma unroll
+        for (int i = 0; i < QL; ++i) {
+          // branch-free: slices past k read slice 0 and are zeroed after
+          const int q = gl + i * L;
+          const bool in = q < kq;
+          const int qc = in ? q : 0;
+          a[u][i] = us[row * kq + qc];
+          c[u][i] = vp[qc];
+          if (!in) a[u][i] = make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < UNR; ++u) {
+        float part = 0.0f;
+#pragma unroll
+        for (int i = 0; i < QL; ++i) {
+          part = fmaf(a[u][i].x, c[u][i].x, part);
+          part = fmaf(a[u][i].y, c[u][i].y, part);
+          part = fmaf(a[u][i].z, c[u][i].z, part);
+          part = fmaf(a[u][i].w, c[u][i].w, part);
+        }
+        part += dpp_mov<0xB1>(part);
+        if constexpr (L > 2) part += dpp_mov<0x4E>(part);
+        if constexpr (L > 4) part += dpp_mov<0x141>(part);
+        if constexpr (L > 8) part += dpp_mov<0x140>(part);
+        const float d = (ok[u] && gl == 0) ? x[u] - part : 0.0f;
+        acc = fma((double)d, (double)d, acc);
+      }
+    }
+  }
+  for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
+  if (lane == 0) partials[(int64_t)b * kLdsWaves + wave] = acc;
 }
 
 __global__ void __launch_bounds__(256)
@@ -105,24 +222,58 @@ k_rmse_final(const double *__restrict__ partials, int64_t count, int64_t nnz, do
 
 }  // namespace
 
-size_t rmse_partials_count(int32_t p) { return (size_t)p * kWavesPerGroup; }
+size_t rmse_partials_count(int32_t p) {
+  return (size_t)p * (size_t)std::max(kRmseSplit * kWavesPerGroup, kLdsWaves);
+}
+
+namespace {
+template <int KP>
+hipError_t launch_rmse_kp(const uint2 *rec, const int64_t *wblock_ptr, const float *U,
+                          const float *V, int64_t n, int64_t m, int32_t k, int32_t p,
+                          double *partials, size_t lds_limit, int64_t *count,
+                          hipStream_t stream) {
+  const Grid G{n, m, p};
+  int64_t rows_max = 0;
+  for (int64_t R = 0; R < p; ++R) rows_max = std::max(rows_max, G.row_start(R + 1) - G.row_start(R));
+  const size_t lds = (size_t)rows_max * (size_t)k * sizeof(float);
+  if (lds <= lds_limit) {
+    static bool attr_set = false;
+    if (!attr_set) {
+      hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&k_rmse_lds<KP>),
+                                         hipFuncAttributeMaxDynamicSharedMemorySize,
+                                         (int)lds_limit);
+      if (e != hipSuccess) return e;
+      attr_set = true;
+    }
+    hipLaunchKernelGGL(k_rmse_lds<KP>, dim3((unsigned)p), dim3(64 * kLdsWaves), lds, stream, rec,
+                       wblock_ptr, U, V, n, m, k, p, partials);
+    *count = (int64_t)p * kLdsWaves;
+  } else {
+    hipLaunchKernelGGL(k_rmse_partial<KP>, dim3((unsigned)(p * kRmseSplit)), dim3(256), 0, stream,
+                       rec, wblock_ptr, U, V, n, m, k, p, partials);
+    *count = (int64_t)p * kRmseSplit * kWavesPerGroup;
+  }
+  return hipGetLastError();
+}
+}  // namespace
 
 hipError_t launch_rmse(const uint2 *rec, const int64_t *wblock_ptr, const float *U,
                        const float *V, int64_t n, int64_t m, int32_t k, int32_t p, int64_t nnz,
-                       double *partials, double *out, hipStream_t stream) {
+                       double *partials, double *out, size_t lds_limit, hipStream_t stream) {
   int kp = 16;
   while (kp < k) kp <<= 1;
-  const dim3 grid((unsigned)p), block(256);
+  int64_t count = 0;
+  hipError_t e;
   switch (kp) {
-    case 16: hipLaunchKernelGGL(k_rmse_partial<16>, grid, block, 0, stream, rec, wblock_ptr, U, V, n, m, k, p, partials); break;
-    case 32: hipLaunchKernelGGL(k_rmse_partial<32>, grid, block, 0, stream, rec, wblock_ptr, U, V, n, m, k, p, partials); break;
-    case 64: hipLaunchKernelGGL(k_rmse_partial<64>, grid, block, 0, stream, rec, wblock_ptr, U, V, n, m, k, p, partials); break;
-    case 128: hipLaunchKernelGGL(k_rmse_partial<128>, grid, block, 0, stream, rec, wblock_ptr, U, V, n, m, k, p, partials); break;
-    case 256: hipLaunchKernelGGL(k_rmse_partial<256>, grid, block, 0, stream, rec, wblock_ptr, U, V, n, m, k, p, partials); break;
+    case 16: e = launch_rmse_kp<16>(rec, wblock_ptr, U, V, n, m, k, p, partials, lds_limit, &count, stream); break;
+    case 32: e = launch_rmse_kp<32>(rec, wblock_ptr, U, V, n, m, k, p, partials, lds_limit, &count, stream); break;
+    case 64: e = launch_rmse_kp<64>(rec, wblock_ptr, U, V, n, m, k, p, partials, lds_limit, &count, stream); break;
+    case 128: e = launch_rmse_kp<128>(rec, wblock_ptr, U, V, n, m, k, p, partials, lds_limit, &count, stream); break;
+    case 256: e = launch_rmse_kp<256>(rec, wblock_ptr, U, V, n, m, k, p, partials, lds_limit, &count, stream); break;
     default: return hipErrorInvalidValue;
   }
-  hipLaunchKernelGGL(k_rmse_final, dim3(1), dim3(256), 0, stream, partials,
-                     (int64_t)rmse_partials_count(p), nnz, out);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_rmse_final, dim3(1), dim3(256), 0, stream, partials, count, nnz, out);
   return hipGetLastError();
 }
 

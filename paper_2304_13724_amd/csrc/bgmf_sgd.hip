@@ -24,6 +24,8 @@
 //     the same sum and the error e needs no broadcast.
 // There is no dense contraction here (each rating is a length-k dot product
 // on a serial dependency chain), so no MFMA is used.
+#include <type_traits>
+
 #include "bgmf_internal.h"
 
 namespace bgmfk {
@@ -68,6 +70,14 @@ __device__ __forceinline__ float buf_ld(__amdgpu_buffer_rsrc_t r, uint32_t voff)
 __device__ __forceinline__ void buf_st(float x, __amdgpu_buffer_rsrc_t r, uint32_t voff) {
   __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(x), r, (int)voff, 0, 0);
 }
+// Same with a wave-uniform scalar offset added (used only with in-range values).
+__device__ __forceinline__ float buf_ld_s(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+  return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, (int)voff, (int)soff, 0));
+}
+__device__ __forceinline__ void buf_st_s(float x, __amdgpu_buffer_rsrc_t r, uint32_t voff,
+                                         uint32_t soff) {
+  __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(x), r, (int)voff, (int)soff, 0);
+}
 
 __device__ __forceinline__ float buf_ld_coherent(__amdgpu_buffer_rsrc_t r, uint32_t voff) {
   return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, (int)voff, 0, kCoherent));
@@ -109,18 +119,16 @@ __device__ __forceinline__ float row_sum(float x) {
 
 // Sum over the lanes that hold distinct dimensions, returned as a scalar
 // (the value of lane 63).  KPL = lanes holding one copy (16, 32 or 64).
-// The two broadcast steps are written as single DPP adds with a row mask
-// (rows outside the mask keep their value); each is preceded by the two
-// wait states a DPP read of a just-written VGPR needs.
+// After the in-row sums, row_bcast:15 adds the last lane of each row to the
+// next row and row_bcast:31 adds lane 31 to rows 2 and 3 (lanes without a
+// source add 0), so lane 63 ends with rows 0 + 1 + 2 + 3; the other rows
+// hold partial sums that are not used.
 template <int KPL>
 __device__ __forceinline__ float lane_total(float x) {
+#pragma clang fp contract(off)
   x = row_sum(x);
-  if constexpr (KPL >= 32)  // rows 1 and 3 add the last lane of rows 0 and 2
-    asm("s_nop 1\n\tv_add_f32_dpp %0, %0, %0 row_bcast:15 row_mask:0xa bank_mask:0xf"
-        : "+v"(x));
-  if constexpr (KPL >= 64)  // rows 2 and 3 add lane 31; lane 63 then holds the total
-    asm("s_nop 1\n\tv_add_f32_dpp %0, %0, %0 row_bcast:31 row_mask:0xc bank_mask:0xf"
-        : "+v"(x));
+  if constexpr (KPL >= 32) x = x + dpp_mov<0x142>(x);  // row_bcast:15
+  if constexpr (KPL >= 64) x = x + dpp_mov<0x143>(x);  // row_bcast:31
   return __uint_as_float((uint32_t)__builtin_amdgcn_readlane(__float_as_int(x), 63));
 }
 
@@ -180,7 +188,9 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
   const uint32_t spare = (uint32_t)P.cols_max * colbytes;
   char *ldsb = reinterpret_cast<char *>(lds);
   const int64_t *wbp = P.wblock_ptr + (int64_t)b * P.p;
-  const float alpha = P.alpha;
+  // alpha is kept in a VGPR so that alpha * e (e is a scalar) is one instruction
+  float alpha;
+  asm("v_mov_b32 %0, %1" : "=v"(alpha) : "s"(P.alpha));
   const float shrink = 1.0f - P.alpha * P.beta;  // u + a(e v - b u) = (1 - a b) u + (a e) v
   const float xscale = 1.0f / (float)KPL;
 
@@ -194,14 +204,15 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
     const uint2 *rp = P.rec + beg;
 
     // Decoded window of 64 records starting at chunk position c:
-    //   wrow = byte offset of the row in U (kOff past the block end)
+    //   wrow = byte offset of the row in U (row 0 past the block end, so the
+    //          value is always a valid scalar offset for a prefetch)
     //   wcol = byte offset of the column slot in LDS (spare past the end)
     //   wx   = x / KPL
-    uint32_t wrow = kOff, wcol = spare;
+    uint32_t wrow = 0u, wcol = spare;
     float wx = 0.0f;
     auto decode = [&](uint2 w, int32_t c) {
       const bool ok = c + lane < len;
-      wrow = ok ? (w.x & kRowMask) * rowbytes : kOff;
+      wrow = ok ? (w.x & kRowMask) * rowbytes : 0u;
       wcol = ok ? ((w.x >> kColShift) & kColMask) * colbytes : spare;
       wx = __uint_as_float(w.y) * xscale;
     };
@@ -210,13 +221,15 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
     // not depend on V, so they are requested before the wait
     float ring[D][NV];
     uint32_t ringrow[D];
+    uint2 Wn1 = make_uint2(0u, 0u);  // raw records of the next chunk
     if (len > 0) {
       decode(rp[lane], 0);
+      Wn1 = rp[CH + lane];
 #pragma unroll
       for (int j = 0; j < D; ++j) {
         ringrow[j] = rl(wrow, j);
 #pragma unroll
-        for (int v = 0; v < NV; ++v) ring[j][v] = buf_ld(Ures, doff[v] + ringrow[j]);
+        for (int v = 0; v < NV; ++v) ring[j][v] = buf_ld_s(Ures, doff[v], ringrow[j]);
       }
     }
     if (s > P.s_begin) {
@@ -259,9 +272,15 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
       // count outstanding loads inside the loop from its steady state alone.
       __builtin_amdgcn_s_waitcnt(0x0F70);
 
-      for (int32_t c = 0; c < len; c += CH) {
-        // records c .. c+63 are decoded; fetch the next window now
-        const uint2 Wn = rp[c + CH + lane];
+      // One chunk of CH ratings, fully unrolled.  In a full chunk every
+      // step is a real rating and U is addressed with the row as a scalar
+      // offset; the last, partial chunk of a block sends the U store of each
+      // step past the end to an out-of-range vector offset (dropped).
+      auto chunk = [&](auto tail_tag, int32_t c) {
+        constexpr bool TAIL = decltype(tail_tag)::value;
+        // records c .. c+63 are decoded and those of chunk c+CH are in
+        // flight; fetch the window two chunks ahead now
+        const uint2 Wn2 = rp[c + 2 * CH + lane];
         uint32_t ccur = rl(wcol, 0);
 #pragma unroll
         for (int j = 0; j < CH; ++j) {
@@ -292,10 +311,14 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
             nu[v] = fmaf(ae, vv[v], shrink * u[v]);
             nv[v] = fmaf(ae, u[v], shrink * vv[v]);
           }
+          const uint32_t row_st = (!TAIL || c + j < len) ? row : kOff;
 #pragma unroll
           for (int v = 0; v < NV; ++v) {
             lds_at(ldsb, waddr + 256u * v) = nv[v];
-            buf_st(nu[v], Ures, doff[v] + row);
+            if constexpr (TAIL)
+              buf_st(nu[v], Ures, doff[v] + row_st);
+            else
+              buf_st_s(nu[v], Ures, doff[v], row);
             uprev[v] = nu[v];
             vnext[v] = (col1 == ccur) ? nv[v] : vl[v];
           }
@@ -305,10 +328,14 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
           // prefetch the u row of rating t + D into the slot just freed
           ringrow[j] = rl(wrow, j + D);
 #pragma unroll
-          for (int v = 0; v < NV; ++v) ring[j][v] = buf_ld(Ures, doff[v] + ringrow[j]);
+          for (int v = 0; v < NV; ++v) ring[j][v] = buf_ld_s(Ures, doff[v], ringrow[j]);
         }
-        decode(Wn, c + CH);
-      }
+        decode(Wn1, c + CH);
+        Wn1 = Wn2;
+      };
+      const int32_t full = len & ~(CH - 1);
+      for (int32_t c = 0; c < full; c += CH) chunk(std::false_type{}, c);
+      if (full < len) chunk(std::true_type{}, full);
       // publish the column slice, 16 columns per round
       for (int cb = 0; cb < ncols; cb += 16) {
         float tmp[16][NV];
