@@ -24,6 +24,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+SWEEP_SRC = os.path.join(ROOT, "paper_2304_13724_amd", "csrc", "bgmf_sgd.hip")
+TRAFFIC_JSON = os.path.join(ROOT, "profiles", "sgd_large_k64_p1024_traffic.json")
 METRIC = "SGD rating updates/sec per epoch + achieved HBM GB/s (k=64, 100M ratings)"
 
 
@@ -39,13 +41,63 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle baseline sample (0 disables it)")
     ap.add_argument("--cache", default=os.environ.get("BGMF_WORKLOAD_CACHE", "/tmp/bgmf_cache"))
-    ap.add_argument("--traffic", default=None,
-                    help="JSON file with measured HBM bytes per sweep launch {fetch, write}")
+    ap.add_argument("--traffic", default=TRAFFIC_JSON,
+                    help="JSON with measured HBM bytes per sweep launch (ignored if the sweep "
+                         "source changed since it was measured)")
+    ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="summarise two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of this "
+                         "bench with --calib-copy-mib, then exit")
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="run one plain device copy of this size before the timed region (a "
+                         "known-size reference for hardware byte counters)")
     return ap.parse_args()
 
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
+
+
+def _sha1(path):
+    import hashlib
+    return hashlib.sha1(open(path, "rb").read()).hexdigest()
+
+
+def pmc_summary(fetch_csv, write_csv, calib_mib):
+    """Per-kernel HBM bytes from FETCH_SIZE / WRITE_SIZE (KiB per dispatch),
+    each scaled by what the counter reads for the calibration copy (the
+    first copy dispatch after the fill of the calibration buffer)."""
+    import csv
+    import statistics
+
+    def load(path):
+        rows = list(csv.DictReader(open(path)))
+        rows.sort(key=lambda r: int(r["Dispatch_Id"]))
+        calib = None
+        for i, r in enumerate(rows):
+            if "FillFunc" in r["Kernel_Name"]:
+                for r2 in rows[i + 1:]:
+                    if "copyBuffer" in r2["Kernel_Name"]:
+                        calib = float(r2["Counter_Value"])
+                        break
+        per = {}
+        for r in rows:
+            per.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]))
+        return calib, per
+
+    true_kib = calib_mib * 1024.0
+    cf, fetch = load(fetch_csv)
+    cw, write = load(write_csv)
+    f_fetch, f_write = true_kib / cf, true_kib / cw
+    out = {"calibration_copy_mib": calib_mib, "fetch_counter_kib": cf, "write_counter_kib": cw,
+           "fetch_scale": f_fetch, "write_scale": f_write, "kernels": {}}
+    for name in sorted(set(fetch) & set(write)):
+        if "bgmfk" not in name:
+            continue
+        fk = statistics.mean(fetch[name]) * f_fetch
+        wk = statistics.mean(write[name]) * f_write
+        out["kernels"][name] = {"dispatches": len(fetch[name]), "fetch_bytes": fk * 1024,
+                                "write_bytes": wk * 1024, "bytes": (fk + wk) * 1024}
+    return out
 
 
 def cpu_baseline(w, budget_s):
@@ -97,6 +149,14 @@ def cpu_baseline(w, budget_s):
 
 def main():
     args = parse()
+    if args.pmc_summary:
+        summ = pmc_summary(args.pmc_summary[0], args.pmc_summary[1], args.calib_copy_mib or 1024)
+        sweep = [v for k, v in summ["kernels"].items() if "k_sgd_lds" in k]
+        res = {"kernel": "k_sgd_lds (one launch = one epoch)", "nnz": int(args.nnz or 100_000_000),
+               "bytes_per_launch": sweep[0]["bytes"] if sweep else None,
+               "sweep_source_sha1": _sha1(SWEEP_SRC), "summary": summ}
+        print(json.dumps(res, indent=1))
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1 "
                           "(multi-GPU sharding is a design note, not built)"}))
@@ -127,6 +187,14 @@ def main():
     log(f"load+bucket {t_load:.2f} s; chain: max col-block {chain[0]}, max row-block {chain[1]}, "
         f"sum of stratum maxima {chain[2]}, non-empty blocks {chain[3]}")
 
+    if args.calib_copy_mib > 0:
+        n_el = args.calib_copy_mib * (1 << 20) // 4
+        src = torch.ones(n_el, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"calibration copy: {args.calib_copy_mib} MiB read + {args.calib_copy_mib} MiB written")
+        del src, dst
     for _ in range(args.warmup):
         mdl.epoch(w.alpha, w.beta)
         mdl.rmse()
@@ -159,7 +227,8 @@ def main():
     traffic = None
     if args.traffic and os.path.exists(args.traffic):
         tr = json.load(open(args.traffic))
-        traffic = tr.get("bytes_per_launch")
+        if tr.get("sweep_source_sha1") == _sha1(SWEEP_SRC) and tr.get("nnz") == w.nnz:
+            traffic = tr.get("bytes_per_launch")
     cpu = cpu_baseline(w, args.cpu_seconds) if args.cpu_seconds > 0 else None
     out = {
         "metric": METRIC,
