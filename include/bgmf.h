@@ -58,6 +58,7 @@ extern "C" {
 #define BGMF_E_UNSUPPORTED -6 /* shape the kernels do not handle */
 #define BGMF_E_HIP        -7  /* a HIP runtime call failed */
 #define BGMF_E_TIMEOUT    -8  /* a device-side wait between strata exceeded its limit */
+#define BGMF_E_BUDGET     -9  /* the ratings budget cannot hold two strata */
 
 typedef struct bgmf bgmf_t; /* opaque handle */
 
@@ -65,7 +66,7 @@ typedef struct bgmf bgmf_t; /* opaque handle */
  * (Algorithm 1's I = J = p).  Allocates U (n x k) and V (m x k) on the
  * current HIP device.
  *   1 <= n, m < 2^31;  k a multiple of 16 in [16, 256];
- *   1 <= p <= min(n, m, 65535);  ceil(n/p) <= 65536;  ceil(m/p) <= 16384.
+ *   1 <= p <= min(n, m, 8192);  ceil(n/p) <= 65536;  ceil(m/p) <= 16384.
  * Returns NULL on error; the reason is bgmf_last_error(NULL) (per thread). */
 bgmf_t *bgmf_create(int64_t n, int64_t m, int32_t k, int32_t p);
 
@@ -137,6 +138,19 @@ int bgmf_factor_ptrs(bgmf_t *h, float **U_dev, float **V_dev);
                                     (default 10,000,000) */
 #define BGMF_OPT_XCD_REMAP     3 /* 1 (default): place neighbouring row-blocks on
                                     the same XCD; 0: plain workgroup order */
+#define BGMF_OPT_RATINGS_BUDGET 4 /* device bytes the bucketed ratings may occupy
+                                    during epochs; 0 (default) = no limit.  Takes
+                                    effect at the next bgmf_load_coo.  If the
+                                    ratings (8 bytes each) do not fit, they are
+                                    kept in pinned host memory in stratum order
+                                    and streamed one stratum at a time through a
+                                    ring of device slots (at least two strata must
+                                    fit, else BGMF_E_BUDGET); U and V stay
+                                    resident.  This applies the paper's point that
+                                    a block-based sweep only needs the blocks in
+                                    flight on the device (Sections 1.2 and 2.2). */
+#define BGMF_OPT_STREAM_SLOTS  5 /* read-only: number of ring slots when the
+                                    loaded ratings stream from host memory, else 0 */
 int bgmf_set_option(bgmf_t *h, int32_t option, int64_t value);
 int bgmf_get_option(const bgmf_t *h, int32_t option, int64_t *value);
 

@@ -24,10 +24,13 @@ BGMF_E_NOMEM = -5
 BGMF_E_UNSUPPORTED = -6
 BGMF_E_HIP = -7
 BGMF_E_TIMEOUT = -8
+BGMF_E_BUDGET = -9
 
 BGMF_OPT_SCHEDULE = 1
 BGMF_OPT_WAIT_LIMIT_US = 2
 BGMF_OPT_XCD_REMAP = 3
+BGMF_OPT_RATINGS_BUDGET = 4
+BGMF_OPT_STREAM_SLOTS = 5
 
 EXPORTED = (
     "bgmf_create", "bgmf_destroy", "bgmf_last_error", "bgmf_set_stream", "bgmf_set_factors",

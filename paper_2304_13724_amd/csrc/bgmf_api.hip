@@ -48,6 +48,18 @@ struct bgmf {
   bool epoch_timed = false, rmse_timed = false;
   int64_t chain[4] = {0, 0, 0, 0};
   std::string msg;
+  // out-of-core: records in pinned host memory, streamed per stratum
+  int64_t budget = 0;            // device bytes for ratings (0: no limit)
+  bool ooc = false;
+  uint2 *host_rec = nullptr;     // stratum-major records (pinned)
+  int32_t *host_perm = nullptr;  // slot-order input positions (pinned)
+  uint2 *ring = nullptr;         // device slots, each one stratum + kRecPad records
+  int nslots = 0;
+  int64_t slot_recs = 0;
+  std::vector<int64_t> strat;    // p + 1 record offsets of the strata
+  hipStream_t side = nullptr;    // copies into the ring
+  std::vector<hipEvent_t> ready, freed;
+  std::vector<bool> slot_used;
 };
 
 namespace {
@@ -74,13 +86,25 @@ int fail(bgmf_t *h, int code, const char *fmt, ...) {
   } while (0)
 
 void free_layout(bgmf_t *h) {
+  if (h->side) hipStreamSynchronize(h->side);
   hipFree(h->block_ptr);
   hipFree(h->wblock_ptr);
   hipFree(h->perm);
   hipFree(h->rec);
+  hipFree(h->ring);
+  if (h->host_rec) hipHostFree(h->host_rec);
+  if (h->host_perm) hipHostFree(h->host_perm);
+  for (auto ev : h->ready) hipEventDestroy(ev);
+  for (auto ev : h->freed) hipEventDestroy(ev);
+  h->ready.clear();
+  h->freed.clear();
+  h->slot_used.clear();
   h->block_ptr = h->wblock_ptr = nullptr;
   h->perm = nullptr;
-  h->rec = nullptr;
+  h->rec = h->ring = h->host_rec = nullptr;
+  h->host_perm = nullptr;
+  h->nslots = 0;
+  h->ooc = false;
   h->nnz = 0;
   h->loaded = false;
 }
@@ -223,6 +247,7 @@ void bgmf_destroy(bgmf_t *h) {
   for (auto &ev : h->ev)
     if (ev) hipEventDestroy(ev);
   if (h->own_stream) hipStreamDestroy(h->own_stream);
+  if (h->side) hipStreamDestroy(h->side);
   delete h;
 }
 
@@ -312,8 +337,11 @@ int bgmf_load_coo(bgmf_t *h, const int32_t *rows, const int32_t *cols, const flo
                           h->stream));
   BucketOut out{h->block_ptr, h->wblock_ptr, h->perm, h->rec};
   LOAD_TRY(hipMemsetAsync(h->err, 0, sizeof(int32_t), h->stream));
-  LOAD_TRY(bucket(d_rows, d_cols, d_vals, nnz, h->n, h->m, h->p, /*flag_v_reload=*/false, scratch,
-                  scratch_bytes, out, h->err, h->stream));
+  // ratings that do not fit the budget are kept stratum-major, so that each
+  // stratum is one contiguous range to stream
+  const bool ooc = h->budget > 0 && (nnz + kRecPad) * (int64_t)sizeof(uint2) > h->budget;
+  LOAD_TRY(bucket(d_rows, d_cols, d_vals, nnz, h->n, h->m, h->p, ooc, scratch, scratch_bytes, out,
+                  h->err, h->stream));
   LOAD_TRY(hipStreamSynchronize(h->stream));
   cleanup();
 #undef LOAD_TRY
@@ -355,6 +383,46 @@ int bgmf_load_coo(bgmf_t *h, const int32_t *rows, const int32_t *cols, const flo
   h->chain[2] = barrier;
   h->chain[3] = nonempty;
 
+  if (ooc) {
+    h->strat.assign((size_t)h->p + 1, 0);
+    int64_t widest = 0;
+    for (int64_t s2 = 0; s2 <= h->p; ++s2) h->strat[s2] = bp[s2 * h->p];
+    for (int64_t s2 = 0; s2 < h->p; ++s2) widest = std::max(widest, h->strat[s2 + 1] - h->strat[s2]);
+    h->slot_recs = widest + kRecPad;
+    const int64_t slot_bytes = h->slot_recs * (int64_t)sizeof(uint2);
+    const int64_t fit = h->budget / slot_bytes;
+    if (fit < 2) {
+      free_layout(h);
+      return fail(h, BGMF_E_BUDGET,
+                  "ratings budget of %lld bytes holds fewer than two strata (the widest stratum "
+                  "needs %lld bytes)",
+                  (long long)h->budget, (long long)slot_bytes);
+    }
+    h->nslots = (int)std::min<int64_t>(fit, h->p);
+    if (!h->side) HIP_TRY(h, hipStreamCreateWithFlags(&h->side, hipStreamNonBlocking));
+    HIP_TRY(h, hipHostMalloc(reinterpret_cast<void **>(&h->host_rec),
+                             (size_t)nnz * sizeof(uint2), hipHostMallocDefault));
+    HIP_TRY(h, hipHostMalloc(reinterpret_cast<void **>(&h->host_perm),
+                             (size_t)nnz * sizeof(int32_t), hipHostMallocDefault));
+    HIP_TRY(h, hipMemcpy(h->host_rec, h->rec, (size_t)nnz * sizeof(uint2), hipMemcpyDeviceToHost));
+    HIP_TRY(h, hipMemcpy(h->host_perm, h->perm, (size_t)nnz * sizeof(int32_t),
+                         hipMemcpyDeviceToHost));
+    hipFree(h->rec);
+    hipFree(h->perm);
+    h->rec = nullptr;
+    h->perm = nullptr;
+    HIP_TRY(h, hipMalloc(&h->ring, (size_t)h->nslots * (size_t)slot_bytes));
+    HIP_TRY(h, hipMemset(h->ring, 0, (size_t)h->nslots * (size_t)slot_bytes));
+    h->ready.assign(h->nslots, nullptr);
+    h->freed.assign(h->nslots, nullptr);
+    h->slot_used.assign(h->nslots, false);
+    for (int i = 0; i < h->nslots; ++i) {
+      HIP_TRY(h, hipEventCreateWithFlags(&h->ready[i], hipEventDisableTiming));
+      HIP_TRY(h, hipEventCreateWithFlags(&h->freed[i], hipEventDisableTiming));
+    }
+    h->ooc = true;
+  }
+
   HIP_TRY(h, hipMemsetAsync(h->flags, 0, (size_t)h->p * kFlagStride * sizeof(int64_t), h->stream));
   HIP_TRY(h, hipStreamSynchronize(h->stream));
   h->epochs_done = 0;
@@ -362,6 +430,33 @@ int bgmf_load_coo(bgmf_t *h, const int32_t *rows, const int32_t *cols, const flo
   h->loaded = true;
   return BGMF_OK;
 }
+
+namespace {
+
+// Out-of-core streaming of stratum s into its ring slot on the side stream;
+// returns the slot's device records.  The copy waits until the kernel that
+// last read the slot has finished, and the caller's stream waits for the copy.
+int stage_stratum(bgmf_t *h, int64_t s, const uint2 **slot_rec) {
+  const int slot = (int)(s % h->nslots);
+  uint2 *dst = h->ring + (size_t)slot * (size_t)h->slot_recs;
+  const int64_t count = h->strat[s + 1] - h->strat[s];
+  if (h->slot_used[slot]) HIP_TRY(h, hipStreamWaitEvent(h->side, h->freed[slot], 0));
+  HIP_TRY(h, hipMemcpyAsync(dst, h->host_rec + h->strat[s], (size_t)count * sizeof(uint2),
+                            hipMemcpyHostToDevice, h->side));
+  HIP_TRY(h, hipEventRecord(h->ready[slot], h->side));
+  HIP_TRY(h, hipStreamWaitEvent(h->stream, h->ready[slot], 0));
+  *slot_rec = dst;
+  return BGMF_OK;
+}
+
+int release_slot(bgmf_t *h, int64_t s) {
+  const int slot = (int)(s % h->nslots);
+  HIP_TRY(h, hipEventRecord(h->freed[slot], h->stream));
+  h->slot_used[slot] = true;
+  return BGMF_OK;
+}
+
+}  // namespace
 
 int bgmf_epoch(bgmf_t *h, float alpha, float beta) {
   if (!h) return BGMF_E_ARG;
@@ -373,7 +468,10 @@ int bgmf_epoch(bgmf_t *h, float alpha, float beta) {
   P.U = h->U;
   P.V = h->V;
   P.rec = h->rec;
-  P.wblock_ptr = h->wblock_ptr;
+  P.blk = h->wblock_ptr;  // wave-major: block (b, s) at b*p + s
+  P.stride_b = h->p;
+  P.stride_s = 1;
+  P.rec_origin = 0;
   P.flags = h->flags;
   P.err = h->err;
   P.n = h->n;
@@ -386,9 +484,26 @@ int bgmf_epoch(bgmf_t *h, float alpha, float beta) {
   P.alpha = alpha;
   P.beta = beta;
   P.xcd_remap = (int32_t)h->xcd_remap;
-  const bool persistent = h->schedule == 0 && h->coop_ok;
   HIP_TRY(h, hipEventRecord(h->ev[0], h->stream));
-  if (persistent) {
+  if (h->ooc) {
+    // one launch per stratum, each reading its stratum from a ring slot
+    P.blk = h->block_ptr;  // stratum-major: block (b, s) at s*p + b
+    P.stride_b = 1;
+    P.stride_s = h->p;
+    for (int64_t s = 0; s < h->p; ++s) {
+      if (h->strat[s + 1] == h->strat[s]) continue;  // empty stratum
+      const uint2 *slot_rec = nullptr;
+      int rc = stage_stratum(h, s, &slot_rec);
+      if (rc != BGMF_OK) return rc;
+      P.rec = slot_rec;
+      P.rec_origin = h->strat[s];
+      P.s_begin = (int32_t)s;
+      P.s_end = (int32_t)s + 1;
+      HIP_TRY(h, launch_sgd(P, h->kp, h->wpg, false, h->lds_bytes, h->stream));
+      rc = release_slot(h, s);
+      if (rc != BGMF_OK) return rc;
+    }
+  } else if (h->schedule == 0 && h->coop_ok) {
     P.s_begin = 0;
     P.s_end = h->p;
     HIP_TRY(h, launch_sgd(P, h->kp, h->wpg, true, h->lds_bytes, h->stream));
@@ -411,8 +526,23 @@ int bgmf_rmse(bgmf_t *h, double *out) {
   if (!h->loaded) return fail(h, BGMF_E_STATE, "bgmf_rmse: no ratings loaded");
   if (!h->factors_set) return fail(h, BGMF_E_STATE, "bgmf_rmse: factors not set");
   HIP_TRY(h, hipEventRecord(h->ev[2], h->stream));
-  HIP_TRY(h, launch_rmse(h->rec, h->wblock_ptr, h->U, h->V, h->n, h->m, h->k, h->p, h->nnz,
-                         h->partials, h->d_rmse, h->lds_limit, h->stream));
+  if (h->ooc) {
+    HIP_TRY(h, rmse_stratum_begin(h->partials, h->p, h->stream));
+    for (int64_t s = 0; s < h->p; ++s) {
+      if (h->strat[s + 1] == h->strat[s]) continue;
+      const uint2 *slot_rec = nullptr;
+      int rc = stage_stratum(h, s, &slot_rec);
+      if (rc != BGMF_OK) return rc;
+      HIP_TRY(h, rmse_stratum_add(slot_rec, h->strat[s], h->block_ptr, (int32_t)s, h->U, h->V,
+                                  h->n, h->m, h->k, h->p, h->partials, h->stream));
+      rc = release_slot(h, s);
+      if (rc != BGMF_OK) return rc;
+    }
+    HIP_TRY(h, rmse_stratum_end(h->partials, h->p, h->nnz, h->d_rmse, h->stream));
+  } else {
+    HIP_TRY(h, launch_rmse(h->rec, h->wblock_ptr, h->U, h->V, h->n, h->m, h->k, h->p, h->nnz,
+                           h->partials, h->d_rmse, h->lds_limit, h->stream));
+  }
   HIP_TRY(h, hipEventRecord(h->ev[3], h->stream));
   h->rmse_timed = true;
   double r = 0.0;
@@ -441,7 +571,9 @@ int bgmf_get_layout(bgmf_t *h, int64_t *block_ptr, int32_t *perm) {
     HIP_TRY(h, hipMemcpyAsync(block_ptr, h->block_ptr,
                               (size_t)((int64_t)h->p * h->p + 1) * sizeof(int64_t),
                               hipMemcpyDeviceToHost, h->stream));
-  if (perm)
+  if (perm && h->ooc)
+    std::memcpy(perm, h->host_perm, (size_t)h->nnz * sizeof(int32_t));
+  else if (perm)
     HIP_TRY(h, hipMemcpyAsync(perm, h->perm, (size_t)h->nnz * sizeof(int32_t),
                               hipMemcpyDeviceToHost, h->stream));
   return sync_checked(h);
@@ -474,6 +606,12 @@ int bgmf_set_option(bgmf_t *h, int32_t option, int64_t value) {
       if (value != 0 && value != 1) return fail(h, BGMF_E_ARG, "xcd remap must be 0 or 1");
       h->xcd_remap = value;
       return BGMF_OK;
+    case BGMF_OPT_RATINGS_BUDGET:
+      if (value < 0) return fail(h, BGMF_E_ARG, "ratings budget must be >= 0");
+      h->budget = value;
+      return BGMF_OK;
+    case BGMF_OPT_STREAM_SLOTS:
+      return fail(h, BGMF_E_ARG, "BGMF_OPT_STREAM_SLOTS is read-only");
     default:
       return fail(h, BGMF_E_ARG, "unknown option %d", option);
   }
@@ -485,6 +623,8 @@ int bgmf_get_option(const bgmf_t *h, int32_t option, int64_t *value) {
     case BGMF_OPT_SCHEDULE: *value = h->schedule; return BGMF_OK;
     case BGMF_OPT_WAIT_LIMIT_US: *value = h->wait_us; return BGMF_OK;
     case BGMF_OPT_XCD_REMAP: *value = h->xcd_remap; return BGMF_OK;
+    case BGMF_OPT_RATINGS_BUDGET: *value = h->budget; return BGMF_OK;
+    case BGMF_OPT_STREAM_SLOTS: *value = h->ooc ? h->nslots : 0; return BGMF_OK;
     default: return BGMF_E_ARG;
   }
 }

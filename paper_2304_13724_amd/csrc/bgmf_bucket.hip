@@ -249,7 +249,7 @@ __global__ void k_transpose(const int64_t *__restrict__ count, int32_t p,
 __global__ void k_gather(const uint64_t *__restrict__ skeys, const int32_t *__restrict__ perm,
                          const int32_t *__restrict__ cols, const float *__restrict__ vals,
                          int64_t nnz, Grid G, int rbits, const int64_t *__restrict__ block_ptr,
-                         const int64_t *__restrict__ wblock_ptr, bool flag_v_reload,
+                         const int64_t *__restrict__ wblock_ptr, bool stratum_major,
                          uint2 *__restrict__ rec, int32_t *err) {
   const uint64_t rmask = (rbits == 0) ? 0ull : ((1ull << rbits) - 1ull);
   for (int64_t t = gid(); t < nnz; t += (int64_t)gridDim.x * blockDim.x) {
@@ -270,23 +270,9 @@ __global__ void k_gather(const uint64_t *__restrict__ skeys, const int32_t *__re
     const int32_t j = cols[e];
     const uint32_t lcol = (uint32_t)(j - G.col_start(C));
     const int64_t beg = block_ptr[q];
-    uint32_t flags = 0;
-    if (flag_v_reload) {
-      // v_j of this rating was last written by a rating 2..kPrefetch-1
-      // positions earlier in the same block (and not by the previous one):
-      // a copy of v_j fetched kPrefetch ratings ahead is stale.
-      const bool prev_same = (t - 1 >= beg) && cols[perm[t - 1]] == j;
-      if (!prev_same) {
-        for (int d = 2; d < kPrefetch && t - d >= beg; ++d)
-          if (cols[perm[t - d]] == j) {
-            flags |= kFlagVReload;
-            break;
-          }
-      }
-    }
-    const int64_t pos = wblock_ptr[b * G.p + s] + (t - beg);
+    const int64_t pos = stratum_major ? t : wblock_ptr[b * G.p + s] + (t - beg);
     if (pos >= 0 && pos < nnz && t >= beg && t < block_ptr[q + 1])
-      rec[pos] = make_uint2(lrow | (lcol << kColShift) | flags, __float_as_uint(vals[e]));
+      rec[pos] = make_uint2(lrow | (lcol << kColShift), __float_as_uint(vals[e]));
     else
       atomicOr(err, kErrLayout);
   }
@@ -319,7 +305,7 @@ size_t bucket_scratch_bytes(int64_t nnz, int32_t p) {
 }
 
 hipError_t bucket(const int32_t *rows, const int32_t *cols, const float *vals, int64_t nnz,
-                  int64_t n, int64_t m, int32_t p, bool flag_v_reload, void *scratch,
+                  int64_t n, int64_t m, int32_t p, bool stratum_major, void *scratch,
                   size_t scratch_bytes, const BucketOut &out, int32_t *err, hipStream_t st) {
   Grid G{n, m, p};
   const int64_t slots = (int64_t)p * p;
@@ -384,7 +370,7 @@ hipError_t bucket(const int32_t *rows, const int32_t *cols, const float *vals, i
   hipLaunchKernelGGL(k_fill_rec, dim3(1), dim3(kThreads), 0, st, out.rec + nnz,
                      (int64_t)kRecPad);
   hipLaunchKernelGGL(k_gather, dim3(g), dim3(kThreads), 0, st, kin, vin, cols, vals, nnz, G,
-                     rbits, out.block_ptr, out.wblock_ptr, flag_v_reload, out.rec, err);
+                     rbits, out.block_ptr, out.wblock_ptr, stratum_major, out.rec, err);
   return hipGetLastError();
 }
 

@@ -17,7 +17,6 @@ constexpr int kColShift = 16;
 constexpr int kColBits = 14;
 constexpr uint32_t kRowMask = (1u << kRowBits) - 1u;
 constexpr uint32_t kColMask = (1u << kColBits) - 1u;
-constexpr uint32_t kFlagVReload = 1u << 30;  // v_j was updated 2..kPrefetch-1 ratings ago
 #ifndef BGMF_PREFETCH
 #define BGMF_PREFETCH 16
 #endif
@@ -41,8 +40,11 @@ struct Grid {
 struct SgdParams {
   float *U;                  // n x k, plus one spare row (index n)
   float *V;                  // m x k
-  const uint2 *rec;          // wave-major rating records (+ kRecPad)
-  const int64_t *wblock_ptr; // [p*p + 1]: start of block (b, s) at index b*p + s
+  const uint2 *rec;          // rating records (+ kRecPad readable past the last one used)
+  const int64_t *blk;        // block offsets: block (b, s) is records
+                             // [blk[x], blk[x + 1]) with x = b*stride_b + s*stride_s
+  int64_t stride_b, stride_s;
+  int64_t rec_origin;        // record of offset blk[x] is rec[blk[x] - rec_origin]
   int64_t *flags;            // [p * kFlagStride]: strata completed by each row-block
   int32_t *err;              // device error word (0 = ok)
   int64_t n, m;
@@ -71,6 +73,15 @@ hipError_t sgd_set_lds_limit(int kp, bool mask, size_t lds_bytes);
 hipError_t launch_rmse(const uint2 *rec, const int64_t *wblock_ptr, const float *U,
                        const float *V, int64_t n, int64_t m, int32_t k, int32_t p, int64_t nnz,
                        double *partials, double *out, size_t lds_limit, hipStream_t stream);
+// Out-of-core pieces of the RMSE pass: zero the per-row-block sums, add the
+// squared errors of stratum s (records of block (b, s) at
+// rec[block_ptr[s*p + b] - rec_origin]), and finish.
+hipError_t rmse_stratum_begin(double *partials, int32_t p, hipStream_t stream);
+hipError_t rmse_stratum_add(const uint2 *rec, int64_t rec_origin, const int64_t *block_ptr,
+                            int32_t s, const float *U, const float *V, int64_t n, int64_t m,
+                            int32_t k, int32_t p, double *partials, hipStream_t stream);
+hipError_t rmse_stratum_end(const double *partials, int32_t p, int64_t nnz, double *out,
+                            hipStream_t stream);
 size_t rmse_partials_count(int32_t p);
 
 // Bucketing: from device COO to the block layout.  Scratch buffers are
@@ -82,8 +93,10 @@ struct BucketOut {
   uint2 *rec;           // [nnz + kRecPad] wave-major records
 };
 size_t bucket_scratch_bytes(int64_t nnz, int32_t p);
+// stratum_major: records in slot order (each stratum contiguous) instead of
+// wave-major order.
 hipError_t bucket(const int32_t *rows, const int32_t *cols, const float *vals, int64_t nnz,
-                  int64_t n, int64_t m, int32_t p, bool flag_v_reload, void *scratch,
+                  int64_t n, int64_t m, int32_t p, bool stratum_major, void *scratch,
                   size_t scratch_bytes, const BucketOut &out, int32_t *err, hipStream_t stream);
 
 }  // namespace bgmfk

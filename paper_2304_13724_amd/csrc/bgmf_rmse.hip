@@ -109,6 +109,86 @@ k_rmse_partial(const uint2 *__restrict__ rec, const int64_t *__restrict__ wblock
   if (lane == 0) partials[(int64_t)blockIdx.x * kWavesPerGroup + wave] = acc;
 }
 
+// Out-of-core RMSE: one wave per row-block b adds the squared errors of
+// block (b, s) of one stratum to partials[b] (each partial is owned by one
+// wave per launch, and launches are ordered on the stream).
+template <int KP>
+__global__ void __launch_bounds__(256)
+k_rmse_stratum(const uint2 *__restrict__ rec, int64_t rec_origin,
+               const int64_t *__restrict__ block_ptr, int32_t s, const float *__restrict__ U,
+               const float *__restrict__ V, int64_t n, int64_t m, int32_t k, int32_t p,
+               double *__restrict__ partials) {
+  constexpr int L = KP >= 64 ? 16 : KP / 4;
+  constexpr int RPS = 64 / L;
+  constexpr int Q = KP / 4;
+  constexpr int QL = (Q + L - 1) / L;
+  constexpr int UNR = 8;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int gl = lane % L, grp = lane / L;
+  const int b = blockIdx.x * kWavesPerGroup + wave;
+  if (b >= p) return;
+  const Grid G{n, m, p};
+  const float *Ub = U + G.row_start(b) * k;
+  const uint32_t rmax = (uint32_t)(G.row_start(b + 1) - G.row_start(b)) - 1u;
+  const int kq = k / 4;
+  const int64_t beg = block_ptr[(int64_t)s * p + b] - rec_origin;
+  const int64_t end = block_ptr[(int64_t)s * p + b + 1] - rec_origin;
+  const int C = (b + s) % p;
+  const float *Vb = V + G.col_start(C) * k;
+  const uint32_t cmax = (uint32_t)(G.col_start(C + 1) - G.col_start(C)) - 1u;
+  double acc = 0.0;
+  for (int64_t t0 = beg; t0 < end; t0 += RPS * UNR) {
+    float4 a[UNR][QL], c[UNR][QL];
+    float x[UNR];
+    bool ok[UNR];
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) {
+      const int64_t t = t0 + u * RPS + grp;
+      ok[u] = t < end;
+      const uint2 r = rec[ok[u] ? t : beg];
+      x[u] = __uint_as_float(r.y);
+      const uint32_t row = min(r.x & kRowMask, rmax);
+      const uint32_t col = min((r.x >> kColShift) & kColMask, cmax);
+      const float4 *up = reinterpret_cast<const float4 *>(Ub + (int64_t)row * k);
+      const float4 *vp = reinterpret_cast<const float4 *>(Vb + (int64_t)col * k);
+#pragma unroll
+      for (int i = 0; i < QL; ++i) {
+        const int q = gl + i * L;
+        const bool in = q < kq;
+        const int qc = in ? q : 0;
+        a[u][i] = up[qc];
+        c[u][i] = vp[qc];
+        if (!in) a[u][i] = make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) {
+      float part = 0.0f;
+#pragma unroll
+      for (int i = 0; i < QL; ++i) {
+        part = fmaf(a[u][i].x, c[u][i].x, part);
+        part = fmaf(a[u][i].y, c[u][i].y, part);
+        part = fmaf(a[u][i].z, c[u][i].z, part);
+        part = fmaf(a[u][i].w, c[u][i].w, part);
+      }
+      part += dpp_mov<0xB1>(part);
+      if constexpr (L > 2) part += dpp_mov<0x4E>(part);
+      if constexpr (L > 4) part += dpp_mov<0x141>(part);
+      if constexpr (L > 8) part += dpp_mov<0x140>(part);
+      const float d = (ok[u] && gl == 0) ? x[u] - part : 0.0f;
+      acc = fma((double)d, (double)d, acc);
+    }
+  }
+  for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
+  if (lane == 0) partials[b] += acc;
+}
+
+__global__ void k_zero(double *x, int64_t count) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count;
+       i += (int64_t)gridDim.x * blockDim.x)
+    x[i] = 0.0;
+}
+
 // Variant with the row-block's U rows staged in LDS: one workgroup of 16
 // waves per row-block, u_i read from LDS, v_j from global memory (L2).
 // Used when rows x k x 4 bytes fit in LDS.
@@ -256,6 +336,39 @@ hipError_t launch_rmse_kp(const uint2 *rec, const int64_t *wblock_ptr, const flo
   return hipGetLastError();
 }
 }  // namespace
+
+hipError_t rmse_stratum_begin(double *partials, int32_t p, hipStream_t stream) {
+  hipLaunchKernelGGL(k_zero, dim3((unsigned)((p + 255) / 256)), dim3(256), 0, stream, partials,
+                     (int64_t)p);
+  return hipGetLastError();
+}
+
+hipError_t rmse_stratum_add(const uint2 *rec, int64_t rec_origin, const int64_t *block_ptr,
+                            int32_t s, const float *U, const float *V, int64_t n, int64_t m,
+                            int32_t k, int32_t p, double *partials, hipStream_t stream) {
+  int kp = 16;
+  while (kp < k) kp <<= 1;
+  const dim3 grid((unsigned)((p + kWavesPerGroup - 1) / kWavesPerGroup)), block(256);
+#define BGMF_RS(KPV)                                                                          \
+  hipLaunchKernelGGL(k_rmse_stratum<KPV>, grid, block, 0, stream, rec, rec_origin, block_ptr, s, \
+                     U, V, n, m, k, p, partials)
+  switch (kp) {
+    case 16: BGMF_RS(16); break;
+    case 32: BGMF_RS(32); break;
+    case 64: BGMF_RS(64); break;
+    case 128: BGMF_RS(128); break;
+    case 256: BGMF_RS(256); break;
+    default: return hipErrorInvalidValue;
+  }
+#undef BGMF_RS
+  return hipGetLastError();
+}
+
+hipError_t rmse_stratum_end(const double *partials, int32_t p, int64_t nnz, double *out,
+                            hipStream_t stream) {
+  hipLaunchKernelGGL(k_rmse_final, dim3(1), dim3(256), 0, stream, partials, (int64_t)p, nnz, out);
+  return hipGetLastError();
+}
 
 hipError_t launch_rmse(const uint2 *rec, const int64_t *wblock_ptr, const float *U,
                        const float *V, int64_t n, int64_t m, int32_t k, int32_t p, int64_t nnz,

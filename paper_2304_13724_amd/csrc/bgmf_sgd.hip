@@ -187,7 +187,7 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
   const uint32_t vbase = ((uint32_t)wave * (P.cols_max + 1) * KP + dim) * 4u;
   const uint32_t spare = (uint32_t)P.cols_max * colbytes;
   char *ldsb = reinterpret_cast<char *>(lds);
-  const int64_t *wbp = P.wblock_ptr + (int64_t)b * P.p;
+  const int64_t *blk_b = P.blk + (int64_t)b * P.stride_b;
   // alpha is kept in a VGPR so that alpha * e (e is a scalar) is one instruction
   float alpha;
   asm("v_mov_b32 %0, %1" : "=v"(alpha) : "s"(P.alpha));
@@ -199,9 +199,10 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
     const int C = (b + s) % P.p;
     const int64_t c0 = G.col_start(C);
     const int ncols = (int)(G.col_start(C + 1) - c0);
-    const int64_t beg = uniform64(wbp[s]);
-    const int32_t len = (int32_t)(uniform64(wbp[s + 1]) - beg);
-    const uint2 *rp = P.rec + beg;
+    const int64_t *bx = blk_b + (int64_t)s * P.stride_s;
+    const int64_t beg = uniform64(bx[0]);
+    const int32_t len = (int32_t)(uniform64(bx[1]) - beg);
+    const uint2 *rp = P.rec + (beg - P.rec_origin);
 
     // Decoded window of 64 records starting at chunk position c:
     //   wrow = byte offset of the row in U (row 0 past the block end, so the

@@ -1,0 +1,91 @@
+"""Out-of-core streaming: with a ratings budget below the bucketed ratings,
+the records live in pinned host memory and are streamed one stratum at a
+time through a ring of device slots.  Results must be bit-identical to the
+in-core sweep (same per-block arithmetic in the same order) and match the
+oracle."""
+import numpy as np
+import pytest
+
+from helpers import gpu_run, oracle_run, row_rel_err
+from workloads import make, make_config
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-4
+
+
+def _run(w, epochs, budget=0, schedule=0):
+    from paper_2304_13724_amd import bgmf
+    with bgmf.Model(w.n, w.m, w.k, w.p) as mdl:
+        mdl.set_option(bgmf.BGMF_OPT_RATINGS_BUDGET, budget)
+        mdl.set_option(bgmf.BGMF_OPT_SCHEDULE, schedule)
+        mdl.set_factors(w.U0, w.V0)
+        mdl.load_coo(w.rows, w.cols, w.vals)
+        slots = mdl.get_option(bgmf.BGMF_OPT_STREAM_SLOTS)
+        bp, perm = mdl.get_layout()
+        hist = []
+        for _ in range(epochs):
+            mdl.epoch(w.alpha, w.beta)
+            hist.append(mdl.rmse())
+        U, V = mdl.get_factors()
+    return U, V, hist, bp, perm, slots
+
+
+def _stratum_bytes(w):
+    import oracle
+    bp, _ = oracle.bucket(w.n, w.m, w.p, w.rows, w.cols)
+    widest = int(np.diff(bp[:: w.p]).max())
+    return (widest + 256) * 8
+
+
+CASES = {
+    "medium_shape": lambda: make_config("medium", n=7_000, m=1_000, nnz=300_000, p=32),
+    "large_shape": lambda: make_config("large", n=48_000, m=1_800, nnz=1_000_000, p=128),
+    "k128_p64": lambda: make("o", n=5_000, m=2_000, nnz=200_000, k=128, p=64, alpha=0.01,
+                             beta=0.05, epochs=1, seed=31, structure="uniform", values="int5",
+                             rank=4),
+}
+
+
+@pytest.mark.parametrize("case", sorted(CASES))
+@pytest.mark.parametrize("nslots", [2, 3, 7])
+def test_ooc_bit_identical_to_incore(case, nslots):
+    w = CASES[case]()
+    budget = nslots * _stratum_bytes(w) + 100
+    inc = _run(w, 3)
+    ooc = _run(w, 3, budget=budget)
+    assert inc[5] == 0 and ooc[5] == nslots
+    assert np.array_equal(ooc[0], inc[0]) and np.array_equal(ooc[1], inc[1])
+    assert np.array_equal(ooc[3], inc[3]) and np.array_equal(ooc[4], inc[4])
+    for a, b in zip(ooc[2], inc[2]):
+        assert abs(a - b) <= 1e-12 * b
+
+
+def test_ooc_matches_oracle():
+    w = CASES["large_shape"]()
+    U_ref, V_ref, hist_ref, bp_ref, perm_ref = oracle_run(w, 2)
+    U, V, hist, bp, perm, slots = _run(w, 2, budget=2 * _stratum_bytes(w))
+    assert slots == 2
+    assert np.array_equal(bp, bp_ref) and np.array_equal(perm, perm_ref)
+    assert row_rel_err(U, U_ref) <= 2 * TOL and row_rel_err(V, V_ref) <= 2 * TOL
+    for a, b in zip(hist, hist_ref):
+        assert abs(a - b) <= TOL * b
+
+
+def test_ooc_budget_below_two_strata():
+    from paper_2304_13724_amd import bgmf
+    w = CASES["medium_shape"]()
+    with bgmf.Model(w.n, w.m, w.k, w.p) as mdl:
+        mdl.set_option(bgmf.BGMF_OPT_RATINGS_BUDGET, _stratum_bytes(w) + 8)
+        mdl.set_factors(w.U0, w.V0)
+        with pytest.raises(bgmf.BgmfError) as ei:
+            mdl.load_coo(w.rows, w.cols, w.vals)
+        assert ei.value.code == bgmf.BGMF_E_BUDGET
+        with pytest.raises(bgmf.BgmfError) as ei:
+            mdl.epoch(w.alpha, w.beta)
+        assert ei.value.code == bgmf.BGMF_E_STATE
+        # the handle stays usable with a workable budget
+        mdl.set_option(bgmf.BGMF_OPT_RATINGS_BUDGET, 4 * _stratum_bytes(w))
+        mdl.load_coo(w.rows, w.cols, w.vals)
+        mdl.epoch(w.alpha, w.beta)
+        assert np.isfinite(mdl.rmse())
