@@ -131,9 +131,14 @@ int bgmf_sync(bgmf_t *h);
 int bgmf_factor_ptrs(bgmf_t *h, float **U_dev, float **V_dev);
 
 /* Options (bgmf_set_option / bgmf_get_option). */
-#define BGMF_OPT_SCHEDULE      1 /* 0: one persistent launch per epoch whose waves
-                                    hand column-blocks over with device-side
-                                    flags (default); 1: one launch per stratum */
+#define BGMF_OPT_SCHEDULE      1 /* 0 (default): automatic, one persistent launch per
+                                    epoch whose waves hand column-blocks over with
+                                    device-side flags when V is staged in LDS and all
+                                    p waves fit on the device at once, else one
+                                    launch per stratum; 1: one launch per stratum;
+                                    2: persistent whenever the waves fit (with V in
+                                    global memory every V access is then
+                                    device-scope, which is slower) */
 #define BGMF_OPT_WAIT_LIMIT_US 2 /* limit of one device-side wait, microseconds
                                     (default 10,000,000) */
 #define BGMF_OPT_XCD_REMAP     3 /* 1 (default): place neighbouring row-blocks on
@@ -143,14 +148,32 @@ int bgmf_factor_ptrs(bgmf_t *h, float **U_dev, float **V_dev);
                                     effect at the next bgmf_load_coo.  If the
                                     ratings (8 bytes each) do not fit, they are
                                     kept in pinned host memory in stratum order
-                                    and streamed one stratum at a time through a
-                                    ring of device slots (at least two strata must
-                                    fit, else BGMF_E_BUDGET); U and V stay
-                                    resident.  This applies the paper's point that
-                                    a block-based sweep only needs the blocks in
-                                    flight on the device (Sections 1.2 and 2.2). */
+                                    and streamed through a ring of 3 (else 2)
+                                    device slots that split the budget; each slot
+                                    takes a chunk of consecutive strata, copied on
+                                    a side stream while the previous chunk is
+                                    swept.  A slot must hold the widest stratum
+                                    plus 256 records (else BGMF_E_BUDGET); U and V
+                                    stay resident.  This applies the paper's point
+                                    that a block-based sweep only needs the blocks
+                                    in flight on the device (Sections 1.2 and 2.2).
+                                    Results are bit-identical to the in-core sweep. */
 #define BGMF_OPT_STREAM_SLOTS  5 /* read-only: number of ring slots when the
                                     loaded ratings stream from host memory, else 0 */
+#define BGMF_OPT_V_STAGING     6 /* where a wave keeps the column slice of V it
+                                    works on: 0 (default) automatic, 1 staged in
+                                    LDS (BGMF_E_UNSUPPORTED if (ceil(m/p) + 1) x k'
+                                    floats, k' = k rounded up to a power of two,
+                                    exceed the LDS of a workgroup), 2 global
+                                    memory.  Automatic picks LDS when the slice
+                                    fits with all p waves resident at once.
+                                    Results are bit-identical either way. */
+#define BGMF_OPT_PLACEMENT     7 /* read-only: how the next epoch runs, bits:
+                                    1 = V slice in LDS, 2 = V in global memory,
+                                    4 = one persistent launch (else one launch per
+                                    stratum) */
+#define BGMF_OPT_STREAM_CHUNKS 8 /* read-only: chunks of strata streamed per epoch
+                                    when the ratings stream from host memory, else 0 */
 int bgmf_set_option(bgmf_t *h, int32_t option, int64_t value);
 int bgmf_get_option(const bgmf_t *h, int32_t option, int64_t *value);
 

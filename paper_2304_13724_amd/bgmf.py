@@ -31,6 +31,9 @@ BGMF_OPT_WAIT_LIMIT_US = 2
 BGMF_OPT_XCD_REMAP = 3
 BGMF_OPT_RATINGS_BUDGET = 4
 BGMF_OPT_STREAM_SLOTS = 5
+BGMF_OPT_V_STAGING = 6
+BGMF_OPT_PLACEMENT = 7
+BGMF_OPT_STREAM_CHUNKS = 8
 
 EXPORTED = (
     "bgmf_create", "bgmf_destroy", "bgmf_last_error", "bgmf_set_stream", "bgmf_set_factors",

@@ -35,14 +35,15 @@ struct bgmf {
   double *partials = nullptr, *d_rmse = nullptr;
   int64_t epochs_done = 0;
   bool factors_set = false, loaded = false;
-  // launch shape
+  // launch shapes: V slice staged in LDS (when it fits) and V in global memory
   int cols_max = 0;
-  int wpg = kWavesPerGroup;
-  size_t lds_bytes = 0;
   size_t lds_limit = 0;
-  bool coop_ok = false;
+  bool lds_fits = false;
+  int wpg_lds = 1, wpg_gv = kWavesPerGroup;
+  size_t lds_bytes_lds = 0, lds_bytes_gv = 0;
+  bool coop_lds = false, coop_gv = false;
   // options
-  int64_t schedule = 0, wait_us = 10000000, xcd_remap = 1;
+  int64_t schedule = 0, wait_us = 10000000, xcd_remap = 1, v_staging = 0;
   // timing
   hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
   bool epoch_timed = false, rmse_timed = false;
@@ -53,10 +54,11 @@ struct bgmf {
   bool ooc = false;
   uint2 *host_rec = nullptr;     // stratum-major records (pinned)
   int32_t *host_perm = nullptr;  // slot-order input positions (pinned)
-  uint2 *ring = nullptr;         // device slots, each one stratum + kRecPad records
+  uint2 *ring = nullptr;         // device slots of slot_recs records each
   int nslots = 0;
   int64_t slot_recs = 0;
   std::vector<int64_t> strat;    // p + 1 record offsets of the strata
+  std::vector<int32_t> chunk;    // chunk c = strata [chunk[c], chunk[c + 1]), one slot each
   hipStream_t side = nullptr;    // copies into the ring
   std::vector<hipEvent_t> ready, freed;
   std::vector<bool> slot_used;
@@ -99,6 +101,7 @@ void free_layout(bgmf_t *h) {
   h->ready.clear();
   h->freed.clear();
   h->slot_used.clear();
+  h->chunk.clear();
   h->block_ptr = h->wblock_ptr = nullptr;
   h->perm = nullptr;
   h->rec = h->ring = h->host_rec = nullptr;
@@ -187,26 +190,33 @@ bgmf_t *bgmf_create(int64_t n, int64_t m, int32_t k, int32_t p) {
       hipSuccess)
     return bail(e, "hipDeviceGetAttribute");
   h->lds_limit = (size_t)lds_max;
-  // the widest workgroup (4, 2 or 1 waves) whose column slices fit in LDS
-  const size_t slice = (size_t)(h->cols_max + 1) * h->kp * sizeof(float);
-  h->wpg = kWavesPerGroup;
-  while (h->wpg > 1 && h->wpg * slice > h->lds_limit) h->wpg >>= 1;
-  h->lds_bytes = h->wpg * slice;
-  if (h->lds_bytes > h->lds_limit) {
-    fail(nullptr, BGMF_E_UNSUPPORTED,
-         "one column-block slice ((%d + 1) columns x %d floats = %zu bytes) exceeds the %zu "
-         "bytes of LDS per workgroup",
-         h->cols_max, h->kp, slice, h->lds_limit);
-    bgmf_destroy(h);
-    return nullptr;
-  }
-  if ((e = sgd_set_lds_limit(h->kp, h->k != h->kp, h->lds_bytes)) != hipSuccess)
-    return bail(e, "hipFuncSetAttribute");
+  // V slice in LDS: the widest workgroup (4, 2 or 1 waves) whose column
+  // slices fit; the persistent schedule needs all p waves resident at once
+  const bool mask = h->k != h->kp;
   int per_cu = 0;
-  if ((e = sgd_occupancy(h->kp, h->k != h->kp, h->wpg, h->lds_bytes, &per_cu)) != hipSuccess)
+  const size_t slice = (size_t)(h->cols_max + 1) * h->kp * sizeof(float);
+  h->wpg_lds = kWavesPerGroup;
+  while (h->wpg_lds > 1 && h->wpg_lds * slice > h->lds_limit) h->wpg_lds >>= 1;
+  h->lds_bytes_lds = h->wpg_lds * slice;
+  h->lds_fits = h->lds_bytes_lds <= h->lds_limit;
+  if (h->lds_fits) {
+    if ((e = sgd_set_lds_limit(h->kp, mask, kVLds, h->lds_bytes_lds)) != hipSuccess)
+      return bail(e, "hipFuncSetAttribute");
+    if ((e = sgd_occupancy(h->kp, mask, kVLds, h->wpg_lds, h->lds_bytes_lds, &per_cu)) !=
+        hipSuccess)
+      return bail(e, "hipOccupancyMaxActiveBlocksPerMultiprocessor");
+    h->coop_lds = (int64_t)per_cu * h->cus >= (p + h->wpg_lds - 1) / h->wpg_lds;
+  }
+  // V in global memory: only a ring of recent results per wave in LDS
+  h->wpg_gv = kWavesPerGroup;
+  h->lds_bytes_gv = h->wpg_gv * sgd_gv_lds_per_wave(h->kp);
+  for (int vm : {kVGlobal, kVGlobalCoherent})
+    if ((e = sgd_set_lds_limit(h->kp, mask, vm, h->lds_bytes_gv)) != hipSuccess)
+      return bail(e, "hipFuncSetAttribute");
+  if ((e = sgd_occupancy(h->kp, mask, kVGlobalCoherent, h->wpg_gv, h->lds_bytes_gv, &per_cu)) !=
+      hipSuccess)
     return bail(e, "hipOccupancyMaxActiveBlocksPerMultiprocessor");
-  const int64_t groups = (p + h->wpg - 1) / h->wpg;
-  h->coop_ok = (int64_t)per_cu * h->cus >= groups;
+  h->coop_gv = (int64_t)per_cu * h->cus >= (p + h->wpg_gv - 1) / h->wpg_gv;
   if ((e = hipStreamCreateWithFlags(&h->own_stream, hipStreamNonBlocking)) != hipSuccess)
     return bail(e, "hipStreamCreate");
   h->stream = h->own_stream;
@@ -388,17 +398,34 @@ int bgmf_load_coo(bgmf_t *h, const int32_t *rows, const int32_t *cols, const flo
     int64_t widest = 0;
     for (int64_t s2 = 0; s2 <= h->p; ++s2) h->strat[s2] = bp[s2 * h->p];
     for (int64_t s2 = 0; s2 < h->p; ++s2) widest = std::max(widest, h->strat[s2 + 1] - h->strat[s2]);
-    h->slot_recs = widest + kRecPad;
-    const int64_t slot_bytes = h->slot_recs * (int64_t)sizeof(uint2);
-    const int64_t fit = h->budget / slot_bytes;
-    if (fit < 2) {
+    // Three slots (copy ahead, compute, drain) if the budget holds three of
+    // the widest stratum, else two; each slot takes a chunk of consecutive
+    // strata, as many as fit, so that one copy and one launch cover many
+    // strata.
+    const int64_t need = widest + kRecPad;
+    h->nslots = 0;
+    for (int cand : {3, 2}) {
+      const int64_t cap = h->budget / ((int64_t)cand * (int64_t)sizeof(uint2));
+      if (cap >= need) {
+        h->nslots = cand;
+        h->slot_recs = cap;
+        break;
+      }
+    }
+    if (h->nslots == 0) {
+      const int64_t slot_bytes = need * (int64_t)sizeof(uint2);
       free_layout(h);
       return fail(h, BGMF_E_BUDGET,
                   "ratings budget of %lld bytes holds fewer than two strata (the widest stratum "
                   "needs %lld bytes)",
                   (long long)h->budget, (long long)slot_bytes);
     }
-    h->nslots = (int)std::min<int64_t>(fit, h->p);
+    h->chunk.assign(1, 0);
+    for (int32_t s2 = 0; s2 < h->p; ++s2)
+      if (h->strat[s2 + 1] - h->strat[h->chunk.back()] + kRecPad > h->slot_recs)
+        h->chunk.push_back(s2);
+    h->chunk.push_back(h->p);
+    const int64_t slot_bytes = h->slot_recs * (int64_t)sizeof(uint2);
     if (!h->side) HIP_TRY(h, hipStreamCreateWithFlags(&h->side, hipStreamNonBlocking));
     HIP_TRY(h, hipHostMalloc(reinterpret_cast<void **>(&h->host_rec),
                              (size_t)nnz * sizeof(uint2), hipHostMallocDefault));
@@ -433,15 +460,17 @@ int bgmf_load_coo(bgmf_t *h, const int32_t *rows, const int32_t *cols, const flo
 
 namespace {
 
-// Out-of-core streaming of stratum s into its ring slot on the side stream;
-// returns the slot's device records.  The copy waits until the kernel that
-// last read the slot has finished, and the caller's stream waits for the copy.
-int stage_stratum(bgmf_t *h, int64_t s, const uint2 **slot_rec) {
-  const int slot = (int)(s % h->nslots);
+// Out-of-core streaming of chunk c (consecutive strata) into its ring slot
+// on the side stream; returns the slot's device records.  The copy waits
+// until the kernels that last read the slot have finished, and the caller's
+// stream waits for the copy.
+int stage_chunk(bgmf_t *h, size_t c, const uint2 **slot_rec) {
+  const int slot = (int)(c % (size_t)h->nslots);
   uint2 *dst = h->ring + (size_t)slot * (size_t)h->slot_recs;
-  const int64_t count = h->strat[s + 1] - h->strat[s];
+  const int64_t first = h->strat[h->chunk[c]];
+  const int64_t count = h->strat[h->chunk[c + 1]] - first;
   if (h->slot_used[slot]) HIP_TRY(h, hipStreamWaitEvent(h->side, h->freed[slot], 0));
-  HIP_TRY(h, hipMemcpyAsync(dst, h->host_rec + h->strat[s], (size_t)count * sizeof(uint2),
+  HIP_TRY(h, hipMemcpyAsync(dst, h->host_rec + first, (size_t)count * sizeof(uint2),
                             hipMemcpyHostToDevice, h->side));
   HIP_TRY(h, hipEventRecord(h->ready[slot], h->side));
   HIP_TRY(h, hipStreamWaitEvent(h->stream, h->ready[slot], 0));
@@ -449,11 +478,35 @@ int stage_stratum(bgmf_t *h, int64_t s, const uint2 **slot_rec) {
   return BGMF_OK;
 }
 
-int release_slot(bgmf_t *h, int64_t s) {
-  const int slot = (int)(s % h->nslots);
+int release_slot(bgmf_t *h, size_t c) {
+  const int slot = (int)(c % (size_t)h->nslots);
   HIP_TRY(h, hipEventRecord(h->freed[slot], h->stream));
   h->slot_used[slot] = true;
   return BGMF_OK;
+}
+
+// Where the sweep keeps V, and how it is launched.  Automatic placement
+// stages the column slice in LDS when it fits with all p waves resident at
+// once, and otherwise leaves V in global memory.  The automatic schedule is
+// persistent for the LDS placement only: with V in global memory a
+// persistent launch needs device-scope V accesses on every update, which
+// cost more than one launch per stratum with plain cached accesses.
+struct SweepShape {
+  bool lds;         // V slice staged in LDS
+  bool persistent;  // one launch for all strata
+  int vmode, wpg;
+  size_t lds_bytes;
+};
+
+SweepShape sweep_shape(const bgmf_t *h) {
+  SweepShape sh{};
+  sh.lds = h->v_staging == 1 || (h->v_staging == 0 && h->lds_fits && h->coop_lds);
+  const bool coop = sh.lds ? h->coop_lds : h->coop_gv;
+  sh.persistent = coop && (h->schedule == 2 || (h->schedule == 0 && sh.lds));
+  sh.vmode = sh.lds ? kVLds : (sh.persistent ? kVGlobalCoherent : kVGlobal);
+  sh.wpg = sh.lds ? h->wpg_lds : h->wpg_gv;
+  sh.lds_bytes = sh.lds ? h->lds_bytes_lds : h->lds_bytes_gv;
+  return sh;
 }
 
 }  // namespace
@@ -484,34 +537,47 @@ int bgmf_epoch(bgmf_t *h, float alpha, float beta) {
   P.alpha = alpha;
   P.beta = beta;
   P.xcd_remap = (int32_t)h->xcd_remap;
+  const SweepShape sh = sweep_shape(h);
   HIP_TRY(h, hipEventRecord(h->ev[0], h->stream));
   if (h->ooc) {
-    // one launch per stratum, each reading its stratum from a ring slot
+    // per chunk of strata in a ring slot: one persistent launch, or one
+    // launch per stratum
     P.blk = h->block_ptr;  // stratum-major: block (b, s) at s*p + b
     P.stride_b = 1;
     P.stride_s = h->p;
-    for (int64_t s = 0; s < h->p; ++s) {
-      if (h->strat[s + 1] == h->strat[s]) continue;  // empty stratum
+    for (size_t c = 0; c + 1 < h->chunk.size(); ++c) {
+      const int32_t s0 = h->chunk[c], s1 = h->chunk[c + 1];
+      if (h->strat[s1] == h->strat[s0]) continue;  // no ratings in these strata
       const uint2 *slot_rec = nullptr;
-      int rc = stage_stratum(h, s, &slot_rec);
+      int rc = stage_chunk(h, c, &slot_rec);
       if (rc != BGMF_OK) return rc;
       P.rec = slot_rec;
-      P.rec_origin = h->strat[s];
-      P.s_begin = (int32_t)s;
-      P.s_end = (int32_t)s + 1;
-      HIP_TRY(h, launch_sgd(P, h->kp, h->wpg, false, h->lds_bytes, h->stream));
-      rc = release_slot(h, s);
+      P.rec_origin = h->strat[s0];
+      if (sh.persistent && s1 - s0 > 1) {
+        P.s_begin = s0;
+        P.s_end = s1;
+        HIP_TRY(h, launch_sgd(P, h->kp, sh.vmode, sh.wpg, true, sh.lds_bytes, h->stream));
+      } else {
+        const int vmode = sh.lds ? kVLds : kVGlobal;
+        for (int32_t s2 = s0; s2 < s1; ++s2) {
+          if (h->strat[s2 + 1] == h->strat[s2]) continue;
+          P.s_begin = s2;
+          P.s_end = s2 + 1;
+          HIP_TRY(h, launch_sgd(P, h->kp, vmode, sh.wpg, false, sh.lds_bytes, h->stream));
+        }
+      }
+      rc = release_slot(h, c);
       if (rc != BGMF_OK) return rc;
     }
-  } else if (h->schedule == 0 && h->coop_ok) {
+  } else if (sh.persistent) {
     P.s_begin = 0;
     P.s_end = h->p;
-    HIP_TRY(h, launch_sgd(P, h->kp, h->wpg, true, h->lds_bytes, h->stream));
+    HIP_TRY(h, launch_sgd(P, h->kp, sh.vmode, sh.wpg, true, sh.lds_bytes, h->stream));
   } else {
     for (int32_t s = 0; s < h->p; ++s) {
       P.s_begin = s;
       P.s_end = s + 1;
-      HIP_TRY(h, launch_sgd(P, h->kp, h->wpg, false, h->lds_bytes, h->stream));
+      HIP_TRY(h, launch_sgd(P, h->kp, sh.vmode, sh.wpg, false, sh.lds_bytes, h->stream));
     }
   }
   HIP_TRY(h, hipEventRecord(h->ev[1], h->stream));
@@ -528,14 +594,15 @@ int bgmf_rmse(bgmf_t *h, double *out) {
   HIP_TRY(h, hipEventRecord(h->ev[2], h->stream));
   if (h->ooc) {
     HIP_TRY(h, rmse_stratum_begin(h->partials, h->p, h->stream));
-    for (int64_t s = 0; s < h->p; ++s) {
-      if (h->strat[s + 1] == h->strat[s]) continue;
+    for (size_t c = 0; c + 1 < h->chunk.size(); ++c) {
+      const int32_t s0 = h->chunk[c], s1 = h->chunk[c + 1];
+      if (h->strat[s1] == h->strat[s0]) continue;
       const uint2 *slot_rec = nullptr;
-      int rc = stage_stratum(h, s, &slot_rec);
+      int rc = stage_chunk(h, c, &slot_rec);
       if (rc != BGMF_OK) return rc;
-      HIP_TRY(h, rmse_stratum_add(slot_rec, h->strat[s], h->block_ptr, (int32_t)s, h->U, h->V,
-                                  h->n, h->m, h->k, h->p, h->partials, h->stream));
-      rc = release_slot(h, s);
+      HIP_TRY(h, rmse_stratum_add(slot_rec, h->strat[s0], h->block_ptr, s0, s1, h->U, h->V, h->n,
+                                  h->m, h->k, h->p, h->partials, h->stream));
+      rc = release_slot(h, c);
       if (rc != BGMF_OK) return rc;
     }
     HIP_TRY(h, rmse_stratum_end(h->partials, h->p, h->nnz, h->d_rmse, h->stream));
@@ -595,7 +662,7 @@ int bgmf_set_option(bgmf_t *h, int32_t option, int64_t value) {
   if (!h) return BGMF_E_ARG;
   switch (option) {
     case BGMF_OPT_SCHEDULE:
-      if (value != 0 && value != 1) return fail(h, BGMF_E_ARG, "schedule must be 0 or 1");
+      if (value < 0 || value > 2) return fail(h, BGMF_E_ARG, "schedule must be 0, 1 or 2");
       h->schedule = value;
       return BGMF_OK;
     case BGMF_OPT_WAIT_LIMIT_US:
@@ -612,6 +679,18 @@ int bgmf_set_option(bgmf_t *h, int32_t option, int64_t value) {
       return BGMF_OK;
     case BGMF_OPT_STREAM_SLOTS:
       return fail(h, BGMF_E_ARG, "BGMF_OPT_STREAM_SLOTS is read-only");
+    case BGMF_OPT_V_STAGING:
+      if (value < 0 || value > 2) return fail(h, BGMF_E_ARG, "V staging must be 0, 1 or 2");
+      if (value == 1 && !h->lds_fits)
+        return fail(h, BGMF_E_UNSUPPORTED,
+                    "a column slice of %d x %d floats does not fit in LDS", h->cols_max + 1,
+                    h->kp);
+      h->v_staging = value;
+      return BGMF_OK;
+    case BGMF_OPT_PLACEMENT:
+      return fail(h, BGMF_E_ARG, "BGMF_OPT_PLACEMENT is read-only");
+    case BGMF_OPT_STREAM_CHUNKS:
+      return fail(h, BGMF_E_ARG, "BGMF_OPT_STREAM_CHUNKS is read-only");
     default:
       return fail(h, BGMF_E_ARG, "unknown option %d", option);
   }
@@ -625,6 +704,15 @@ int bgmf_get_option(const bgmf_t *h, int32_t option, int64_t *value) {
     case BGMF_OPT_XCD_REMAP: *value = h->xcd_remap; return BGMF_OK;
     case BGMF_OPT_RATINGS_BUDGET: *value = h->budget; return BGMF_OK;
     case BGMF_OPT_STREAM_SLOTS: *value = h->ooc ? h->nslots : 0; return BGMF_OK;
+    case BGMF_OPT_V_STAGING: *value = h->v_staging; return BGMF_OK;
+    case BGMF_OPT_STREAM_CHUNKS:
+      *value = h->ooc ? (int64_t)h->chunk.size() - 1 : 0;
+      return BGMF_OK;
+    case BGMF_OPT_PLACEMENT: {
+      const SweepShape sh = sweep_shape(h);
+      *value = (sh.lds ? 1 : 2) | (sh.persistent ? 4 : 0);
+      return BGMF_OK;
+    }
     default: return BGMF_E_ARG;
   }
 }

@@ -61,25 +61,35 @@ constexpr int kWavesPerGroup = 4;
 constexpr int kErrTimeout = 1;
 constexpr int kErrLayout = 2;  // a bucketing write fell outside its array
 
+// Where the sweep keeps the column slice of V it is working on.
+constexpr int kVLds = 0;             // staged in LDS, (cols_max + 1) x kp floats per wave
+constexpr int kVGlobal = 1;          // global memory, plain cached accesses (one stratum per launch)
+constexpr int kVGlobalCoherent = 2;  // global memory, device-scope accesses (persistent launch)
+
 // Launchers (defined in the .hip files); all enqueue on `stream`.
 // One wave per row-block; a workgroup holds waves_per_group (1, 2 or 4)
-// row-blocks, each with its own LDS slice of (cols_max + 1) x kp floats.
-hipError_t launch_sgd(const SgdParams &P, int kp, int waves_per_group, bool cooperative,
+// row-blocks, each with its own LDS area: the column slice (kVLds) or the
+// ring of recent results, sgd_gv_lds_per_wave(kp) bytes (global V).
+hipError_t launch_sgd(const SgdParams &P, int kp, int vmode, int waves_per_group, bool cooperative,
                       size_t lds_bytes, hipStream_t stream);
-hipError_t sgd_occupancy(int kp, bool mask, int waves_per_group, size_t lds_bytes,
+hipError_t sgd_occupancy(int kp, bool mask, int vmode, int waves_per_group, size_t lds_bytes,
                          int *groups_per_cu);
-hipError_t sgd_set_lds_limit(int kp, bool mask, size_t lds_bytes);
+hipError_t sgd_set_lds_limit(int kp, bool mask, int vmode, size_t lds_bytes);
+size_t sgd_gv_lds_per_wave(int kp);
 
 hipError_t launch_rmse(const uint2 *rec, const int64_t *wblock_ptr, const float *U,
                        const float *V, int64_t n, int64_t m, int32_t k, int32_t p, int64_t nnz,
                        double *partials, double *out, size_t lds_limit, hipStream_t stream);
-// Out-of-core pieces of the RMSE pass: zero the per-row-block sums, add the
-// squared errors of stratum s (records of block (b, s) at
-// rec[block_ptr[s*p + b] - rec_origin]), and finish.
+// Out-of-core pieces of the RMSE pass: zero the partial sums
+// (kRmseStrataGroups per row-block), add the squared errors of strata
+// [s0, s1) (records of block (b, s) at rec[block_ptr[s*p + b] - rec_origin]),
+// and finish.
+constexpr int kRmseStrataGroups = 16;
 hipError_t rmse_stratum_begin(double *partials, int32_t p, hipStream_t stream);
 hipError_t rmse_stratum_add(const uint2 *rec, int64_t rec_origin, const int64_t *block_ptr,
-                            int32_t s, const float *U, const float *V, int64_t n, int64_t m,
-                            int32_t k, int32_t p, double *partials, hipStream_t stream);
+                            int32_t s0, int32_t s1, const float *U, const float *V, int64_t n,
+                            int64_t m, int32_t k, int32_t p, double *partials,
+                            hipStream_t stream);
 hipError_t rmse_stratum_end(const double *partials, int32_t p, int64_t nnz, double *out,
                             hipStream_t stream);
 size_t rmse_partials_count(int32_t p);

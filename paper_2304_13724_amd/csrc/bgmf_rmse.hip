@@ -109,15 +109,17 @@ k_rmse_partial(const uint2 *__restrict__ rec, const int64_t *__restrict__ wblock
   if (lane == 0) partials[(int64_t)blockIdx.x * kWavesPerGroup + wave] = acc;
 }
 
-// Out-of-core RMSE: one wave per row-block b adds the squared errors of
-// block (b, s) of one stratum to partials[b] (each partial is owned by one
-// wave per launch, and launches are ordered on the stream).
+// Out-of-core RMSE over the strata [s0, s1) held in one device slot: the
+// wave of row-block b and grid row y adds the squared errors of blocks
+// (b, s), s = s0 + y, s0 + y + gridDim.y, ..., to partials[y p + b] (each
+// partial is owned by one wave per launch, and launches are ordered on the
+// stream).
 template <int KP>
 __global__ void __launch_bounds__(256)
 k_rmse_stratum(const uint2 *__restrict__ rec, int64_t rec_origin,
-               const int64_t *__restrict__ block_ptr, int32_t s, const float *__restrict__ U,
-               const float *__restrict__ V, int64_t n, int64_t m, int32_t k, int32_t p,
-               double *__restrict__ partials) {
+               const int64_t *__restrict__ block_ptr, int32_t s0, int32_t s1,
+               const float *__restrict__ U, const float *__restrict__ V, int64_t n, int64_t m,
+               int32_t k, int32_t p, double *__restrict__ partials) {
   constexpr int L = KP >= 64 ? 16 : KP / 4;
   constexpr int RPS = 64 / L;
   constexpr int Q = KP / 4;
@@ -131,12 +133,13 @@ k_rmse_stratum(const uint2 *__restrict__ rec, int64_t rec_origin,
   const float *Ub = U + G.row_start(b) * k;
   const uint32_t rmax = (uint32_t)(G.row_start(b + 1) - G.row_start(b)) - 1u;
   const int kq = k / 4;
+  double acc = 0.0;
+  for (int32_t s = s0 + (int32_t)blockIdx.y; s < s1; s += (int32_t)gridDim.y) {
   const int64_t beg = block_ptr[(int64_t)s * p + b] - rec_origin;
   const int64_t end = block_ptr[(int64_t)s * p + b + 1] - rec_origin;
   const int C = (b + s) % p;
   const float *Vb = V + G.col_start(C) * k;
   const uint32_t cmax = (uint32_t)(G.col_start(C + 1) - G.col_start(C)) - 1u;
-  double acc = 0.0;
   for (int64_t t0 = beg; t0 < end; t0 += RPS * UNR) {
     float4 a[UNR][QL], c[UNR][QL];
     float x[UNR];
@@ -179,8 +182,9 @@ k_rmse_stratum(const uint2 *__restrict__ rec, int64_t rec_origin,
       acc = fma((double)d, (double)d, acc);
     }
   }
+  }
   for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
-  if (lane == 0) partials[b] += acc;
+  if (lane == 0) partials[(int64_t)blockIdx.y * p + b] += acc;
 }
 
 __global__ void k_zero(double *x, int64_t count) {
@@ -338,20 +342,24 @@ hipError_t launch_rmse_kp(const uint2 *rec, const int64_t *wblock_ptr, const flo
 }  // namespace
 
 hipError_t rmse_stratum_begin(double *partials, int32_t p, hipStream_t stream) {
-  hipLaunchKernelGGL(k_zero, dim3((unsigned)((p + 255) / 256)), dim3(256), 0, stream, partials,
-                     (int64_t)p);
+  const int64_t count = (int64_t)kRmseStrataGroups * p;
+  hipLaunchKernelGGL(k_zero, dim3((unsigned)((count + 255) / 256)), dim3(256), 0, stream, partials,
+                     count);
   return hipGetLastError();
 }
 
 hipError_t rmse_stratum_add(const uint2 *rec, int64_t rec_origin, const int64_t *block_ptr,
-                            int32_t s, const float *U, const float *V, int64_t n, int64_t m,
-                            int32_t k, int32_t p, double *partials, hipStream_t stream) {
+                            int32_t s0, int32_t s1, const float *U, const float *V, int64_t n,
+                            int64_t m, int32_t k, int32_t p, double *partials,
+                            hipStream_t stream) {
   int kp = 16;
   while (kp < k) kp <<= 1;
-  const dim3 grid((unsigned)((p + kWavesPerGroup - 1) / kWavesPerGroup)), block(256);
-#define BGMF_RS(KPV)                                                                          \
-  hipLaunchKernelGGL(k_rmse_stratum<KPV>, grid, block, 0, stream, rec, rec_origin, block_ptr, s, \
-                     U, V, n, m, k, p, partials)
+  const dim3 grid((unsigned)((p + kWavesPerGroup - 1) / kWavesPerGroup),
+                  (unsigned)std::min(kRmseStrataGroups, s1 - s0)),
+      block(256);
+#define BGMF_RS(KPV)                                                                            \
+  hipLaunchKernelGGL(k_rmse_stratum<KPV>, grid, block, 0, stream, rec, rec_origin, block_ptr, s0, \
+                     s1, U, V, n, m, k, p, partials)
   switch (kp) {
     case 16: BGMF_RS(16); break;
     case 32: BGMF_RS(32); break;
@@ -366,7 +374,8 @@ hipError_t rmse_stratum_add(const uint2 *rec, int64_t rec_origin, const int64_t 
 
 hipError_t rmse_stratum_end(const double *partials, int32_t p, int64_t nnz, double *out,
                             hipStream_t stream) {
-  hipLaunchKernelGGL(k_rmse_final, dim3(1), dim3(256), 0, stream, partials, (int64_t)p, nnz, out);
+  hipLaunchKernelGGL(k_rmse_final, dim3(1), dim3(256), 0, stream, partials,
+                     (int64_t)kRmseStrataGroups * p, nnz, out);
   return hipGetLastError();
 }
 

@@ -10,18 +10,19 @@
 // neighbour's progress word (acquire) and publishes its own (release).
 //
 // Per wave and block:
-//   * the block's column slice of V (ncols x k fp32) is copied into LDS after
-//     the acquire, updated there, and written back before the release;
+//   * V: either the block's column slice (ncols x k fp32) is copied into LDS
+//     after the acquire, updated there and written back before the release
+//     (k_sgd_lds), or V stays in global memory and each rating's v row is
+//     prefetched like the u rows (k_sgd_gv, for slices too wide for LDS);
 //   * U rows are owned by the wave for the whole launch; they are prefetched
 //     from HBM kPrefetch ratings ahead into a register ring and stored after
 //     every update (a row that repeats at the next rating is forwarded in
 //     registers instead of re-read);
 //   * ratings are read 64 at a time with one coalesced 512-byte load and
 //     broadcast with v_readlane;
-//   * k is spread over the 64 lanes (one dimension per lane, or k/64 per
-//     lane for k > 64); the dot product is reduced across lanes with DPP row
-//     operations and the gfx950 permlane16/32 swaps, so every lane ends with
-//     the same sum and the error e needs no broadcast.
+//   * k is spread over the 64 lanes, each lane holding k/64 consecutive
+//     dimensions (one 4-, 8- or 16-byte access per row); the dot product is
+//     reduced across lanes with DPP row operations and row broadcasts.
 // There is no dense contraction here (each rating is a length-k dot product
 // on a serial dependency chain), so no MFMA is used.
 #include <type_traits>
@@ -60,30 +61,79 @@ __device__ __forceinline__ int64_t uniform64(int64_t x) {
 constexpr int kCoherent = 16;  // cache-policy bits of a device-scope access (sc1)
 
 // Buffer descriptor word 3 for gfx9 (32-bit data format); accesses whose
-// VGPR offset is at or past num_records return 0 / are dropped.
+// VGPR offset is at or past num_records return 0 / are dropped.  The scalar
+// offset is not range-checked: it only ever carries in-range values.
 constexpr int kBufWord3 = 0x00020000;
 constexpr uint32_t kOff = 0x40000000u;  // outside every buffer, even when added twice
 
-__device__ __forceinline__ float buf_ld(__amdgpu_buffer_rsrc_t r, uint32_t voff) {
-  return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, (int)voff, 0, 0));
-}
-__device__ __forceinline__ void buf_st(float x, __amdgpu_buffer_rsrc_t r, uint32_t voff) {
-  __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(x), r, (int)voff, 0, 0);
-}
-// Same with a wave-uniform scalar offset added (used only with in-range values).
-__device__ __forceinline__ float buf_ld_s(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
-  return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, (int)voff, (int)soff, 0));
-}
-__device__ __forceinline__ void buf_st_s(float x, __amdgpu_buffer_rsrc_t r, uint32_t voff,
-                                         uint32_t soff) {
-  __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(x), r, (int)voff, (int)soff, 0);
+// One lane's share of a factor row: NV consecutive floats, one access.
+template <int NV, int POL>
+__device__ __forceinline__ void ld_row(float (&x)[NV], __amdgpu_buffer_rsrc_t r, uint32_t voff,
+                                       uint32_t soff) {
+  if constexpr (NV == 1) {
+    x[0] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, (int)voff, (int)soff, POL));
+  } else if constexpr (NV == 2) {
+    const auto t = __builtin_amdgcn_raw_buffer_load_b64(r, (int)voff, (int)soff, POL);
+    x[0] = __uint_as_float(t[0]);
+    x[1] = __uint_as_float(t[1]);
+  } else {
+    static_assert(NV == 4, "one lane holds 1, 2 or 4 dimensions");
+    const auto t = __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, (int)soff, POL);
+#pragma unroll
+    for (int v = 0; v < 4; ++v) x[v] = __uint_as_float(t[v]);
+  }
 }
 
-__device__ __forceinline__ float buf_ld_coherent(__amdgpu_buffer_rsrc_t r, uint32_t voff) {
-  return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, (int)voff, 0, kCoherent));
+template <int NV, int POL>
+__device__ __forceinline__ void st_row(const float (&x)[NV], __amdgpu_buffer_rsrc_t r,
+                                       uint32_t voff, uint32_t soff) {
+  if constexpr (NV == 1) {
+    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(x[0]), r, (int)voff, (int)soff, POL);
+  } else if constexpr (NV == 2) {
+    __attribute__((ext_vector_type(2))) unsigned t;
+    t[0] = __float_as_uint(x[0]);
+    t[1] = __float_as_uint(x[1]);
+    __builtin_amdgcn_raw_buffer_store_b64(t, r, (int)voff, (int)soff, POL);
+  } else {
+    __attribute__((ext_vector_type(4))) unsigned t;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) t[v] = __float_as_uint(x[v]);
+    __builtin_amdgcn_raw_buffer_store_b128(t, r, (int)voff, (int)soff, POL);
+  }
 }
-__device__ __forceinline__ void buf_st_coherent(float x, __amdgpu_buffer_rsrc_t r, uint32_t voff) {
-  __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(x), r, (int)voff, 0, kCoherent);
+
+template <int NV>
+struct LdsVec;
+template <>
+struct LdsVec<1> { using T = float; };
+template <>
+struct LdsVec<2> { using T = float2; };
+template <>
+struct LdsVec<4> { using T = float4; };
+
+template <int NV>
+__device__ __forceinline__ void lds_ld(float (&x)[NV], const char *base, uint32_t off) {
+  const auto t = *reinterpret_cast<const typename LdsVec<NV>::T *>(base + off);
+  if constexpr (NV == 1) {
+    x[0] = t;
+  } else {
+    const float *f = reinterpret_cast<const float *>(&t);
+#pragma unroll
+    for (int v = 0; v < NV; ++v) x[v] = f[v];
+  }
+}
+
+template <int NV>
+__device__ __forceinline__ void lds_st(const float (&x)[NV], char *base, uint32_t off) {
+  typename LdsVec<NV>::T t;
+  if constexpr (NV == 1) {
+    t = x[0];
+  } else {
+    float *f = reinterpret_cast<float *>(&t);
+#pragma unroll
+    for (int v = 0; v < NV; ++v) f[v] = x[v];
+  }
+  *reinterpret_cast<typename LdsVec<NV>::T *>(base + off) = t;
 }
 
 // Wait until *flag >= target.  Returns false on timeout.
@@ -132,51 +182,59 @@ __device__ __forceinline__ float lane_total(float x) {
   return __uint_as_float((uint32_t)__builtin_amdgcn_readlane(__float_as_int(x), 63));
 }
 
-__device__ __forceinline__ float &lds_at(char *base, uint32_t byte_off) {
-  return *reinterpret_cast<float *>(base + byte_off);
+// Lane layout shared by both sweeps.  KP: k rounded up to a power of two
+// (>= 16).  For KP >= 64 lane l holds dimensions [l NV, l NV + NV), NV =
+// KP / 64; for KP < 64 lane l holds dimension l mod KP (the 64/KP lane
+// groups hold identical copies, compute the same values and store them to
+// the same addresses).  MASK: k < KP; a lane whose dimensions are >= k holds
+// padding (kept at zero, never stored).  Since k is a multiple of 16, a
+// lane's NV dimensions are all real or all padding.
+template <int KP, bool MASK>
+struct Lanes {
+  static constexpr int NV = KP <= 64 ? 1 : KP / 64;
+  static constexpr int KPL = KP < 64 ? KP : 64;  // lanes holding one copy
+  int lane, first;  // first dimension of the lane
+  uint32_t doff;    // byte offset of that dimension in a row, kOff for padding
+  __device__ __forceinline__ explicit Lanes(int k) {
+    lane = threadIdx.x & 63;
+    first = KP >= 64 ? lane * NV : (lane & (KP - 1));
+    doff = (!MASK || first < k) ? (uint32_t)first * 4u : kOff;
+  }
+};
+
+// Row-block of this wave.  Workgroups are dealt round-robin to the 8 XCDs;
+// with xcd_remap each XCD holds a contiguous range of row-blocks, so that
+// most column-block hand-overs stay inside one L2.
+__device__ __forceinline__ int row_block_of_wave(const SgdParams &P, int wave) {
+  int grp = blockIdx.x;
+  if (P.xcd_remap) {
+    const int G = gridDim.x;
+    grp = (blockIdx.x & 7) * (G >> 3) + (blockIdx.x >> 3);
+  }
+  return grp * (int)(blockDim.x >> 6) + wave;
 }
 
-// KP: k rounded up to a power of two (>= 16).  Lane l holds dimensions
-// dim(l) + 64 v, v < NV, where dim(l) = l for KP >= 64 and l mod KP for
-// KP < 64 (then the 64/KP lane groups hold identical copies, compute the
-// same values and store them to the same addresses).  MASK: k < KP, so the
-// dimensions >= k are padding (kept at zero, never stored).
-//
 // Error term: every lane adds x/KPL to its partial products, so the lane
 // total is e = x - u.v directly (x/KPL is an exact power-of-two scaling).
 template <int KP, bool MASK>
 __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
-  constexpr int NV = KP <= 64 ? 1 : KP / 64;
-  constexpr int KPL = KP < 64 ? KP : 64;
+  using L = Lanes<KP, MASK>;
+  constexpr int NV = L::NV;
+  constexpr int KPL = L::KPL;
   constexpr int D = kPrefetch;
   constexpr int CH = D;  // ratings per unrolled chunk; ring slot = step in chunk
-  const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
-  const int dim = KP >= 64 ? lane : (lane & (KP - 1));
-  int grp = blockIdx.x;
-  if (P.xcd_remap) {
-    // workgroups are dealt round-robin to the 8 XCDs; give each XCD a
-    // contiguous range of row-blocks so that most column-block hand-overs
-    // stay inside one L2
-    const int G = gridDim.x;
-    grp = (blockIdx.x & 7) * (G >> 3) + (blockIdx.x >> 3);
-  }
-  const int b = grp * (int)(blockDim.x >> 6) + wave;
+  const int b = row_block_of_wave(P, wave);
   if (b >= P.p) return;
+  const L ln(P.k);
+  const int lane = ln.lane;
+  const uint32_t doff = ln.doff;
 
   extern __shared__ float lds[];
   const Grid G{P.n, P.m, P.p};
   const int k = P.k;
   const uint32_t rowbytes = (uint32_t)k * 4u;
   const uint32_t colbytes = (uint32_t)KP * 4u;
-  bool act[NV];
-#pragma unroll
-  for (int v = 0; v < NV; ++v) act[v] = !MASK || (dim + 64 * v < k);
-  // byte offset of this lane's dimension v inside a row; padding
-  // dimensions get an out-of-range offset (loads 0, stores dropped)
-  uint32_t doff[NV];
-#pragma unroll
-  for (int v = 0; v < NV; ++v) doff[v] = act[v] ? (uint32_t)(dim + 64 * v) * 4u : kOff;
 
   // U rows of row-block b (owned by this wave for the whole launch)
   const int64_t r0 = G.row_start(b);
@@ -184,7 +242,7 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
   const __amdgpu_buffer_rsrc_t Ures =
       __builtin_amdgcn_make_buffer_rsrc(P.U + r0 * k, (short)0, (int)(rows_b * rowbytes), kBufWord3);
   // this wave's LDS column slots: cols_max real ones and one spare
-  const uint32_t vbase = ((uint32_t)wave * (P.cols_max + 1) * KP + dim) * 4u;
+  const uint32_t vbase = ((uint32_t)wave * (P.cols_max + 1) * KP + ln.first) * 4u;
   const uint32_t spare = (uint32_t)P.cols_max * colbytes;
   char *ldsb = reinterpret_cast<char *>(lds);
   const int64_t *blk_b = P.blk + (int64_t)b * P.stride_b;
@@ -229,8 +287,7 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
 #pragma unroll
       for (int j = 0; j < D; ++j) {
         ringrow[j] = rl(wrow, j);
-#pragma unroll
-        for (int v = 0; v < NV; ++v) ring[j][v] = buf_ld_s(Ures, doff[v], ringrow[j]);
+        ld_row<NV, 0>(ring[j], Ures, doff, ringrow[j]);
       }
     }
     if (s > P.s_begin) {
@@ -243,27 +300,21 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
     }
     if (len > 0) {
       // stage the column slice of V in LDS, 16 columns per round trip
+      // (columns past the slice read 0 and land in the spare slot)
       const __amdgpu_buffer_rsrc_t Vres = __builtin_amdgcn_make_buffer_rsrc(
           P.V + c0 * k, (short)0, (int)((uint32_t)ncols * rowbytes), kBufWord3);
       for (int cb = 0; cb < ncols; cb += 16) {
         float tmp[16][NV];
 #pragma unroll
         for (int i = 0; i < 16; ++i)
+          ld_row<NV, kCoherent>(tmp[i], Vres, doff + (uint32_t)(cb + i) * rowbytes, 0);
 #pragma unroll
-          for (int v = 0; v < NV; ++v)
-            tmp[i][v] = buf_ld_coherent(Vres, doff[v] + (uint32_t)(cb + i) * rowbytes);
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const uint32_t slot = (uint32_t)min(cb + i, P.cols_max);
-#pragma unroll
-          for (int v = 0; v < NV; ++v)
-            lds_at(ldsb, vbase + slot * colbytes + 256u * v) = tmp[i][v];
-        }
+        for (int i = 0; i < 16; ++i)
+          lds_st<NV>(tmp[i], ldsb, vbase + (uint32_t)min(cb + i, P.cols_max) * colbytes);
       }
       uint32_t waddr = vbase + rl(wcol, 0);  // LDS address of the current column
       float vnext[NV];
-#pragma unroll
-      for (int v = 0; v < NV; ++v) vnext[v] = lds_at(ldsb, waddr + 256u * v);
+      lds_ld<NV>(vnext, ldsb, waddr);
       uint32_t prev_row = 0xFFFFFFFFu;
       float uprev[NV];
 #pragma unroll
@@ -299,8 +350,7 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
           // value computed below is forwarded instead
           const uint32_t raddr = vbase + col1;
           float vl[NV];
-#pragma unroll
-          for (int v = 0; v < NV; ++v) vl[v] = lds_at(ldsb, raddr + 256u * v);
+          lds_ld<NV>(vl, ldsb, raddr);
 
           float tpart = fmaf(-u[0], vv[0], x64);
 #pragma unroll
@@ -312,14 +362,13 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
             nu[v] = fmaf(ae, vv[v], shrink * u[v]);
             nv[v] = fmaf(ae, u[v], shrink * vv[v]);
           }
-          const uint32_t row_st = (!TAIL || c + j < len) ? row : kOff;
+          lds_st<NV>(nv, ldsb, waddr);
+          if constexpr (TAIL)
+            st_row<NV, 0>(nu, Ures, doff + ((c + j < len) ? row : kOff), 0);
+          else
+            st_row<NV, 0>(nu, Ures, doff, row);
 #pragma unroll
           for (int v = 0; v < NV; ++v) {
-            lds_at(ldsb, waddr + 256u * v) = nv[v];
-            if constexpr (TAIL)
-              buf_st(nu[v], Ures, doff[v] + row_st);
-            else
-              buf_st_s(nu[v], Ures, doff[v], row);
             uprev[v] = nu[v];
             vnext[v] = (col1 == ccur) ? nv[v] : vl[v];
           }
@@ -328,8 +377,7 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
           waddr = raddr;
           // prefetch the u row of rating t + D into the slot just freed
           ringrow[j] = rl(wrow, j + D);
-#pragma unroll
-          for (int v = 0; v < NV; ++v) ring[j][v] = buf_ld_s(Ures, doff[v], ringrow[j]);
+          ld_row<NV, 0>(ring[j], Ures, doff, ringrow[j]);
         }
         decode(Wn1, c + CH);
         Wn1 = Wn2;
@@ -337,20 +385,16 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
       const int32_t full = len & ~(CH - 1);
       for (int32_t c = 0; c < full; c += CH) chunk(std::false_type{}, c);
       if (full < len) chunk(std::true_type{}, full);
-      // publish the column slice, 16 columns per round
+      // publish the column slice, 16 columns per round (stores past the
+      // slice are dropped)
       for (int cb = 0; cb < ncols; cb += 16) {
         float tmp[16][NV];
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const uint32_t slot = (uint32_t)min(cb + i, P.cols_max);
-#pragma unroll
-          for (int v = 0; v < NV; ++v) tmp[i][v] = lds_at(ldsb, vbase + slot * colbytes + 256u * v);
-        }
+        for (int i = 0; i < 16; ++i)
+          lds_ld<NV>(tmp[i], ldsb, vbase + (uint32_t)min(cb + i, P.cols_max) * colbytes);
 #pragma unroll
         for (int i = 0; i < 16; ++i)
-#pragma unroll
-          for (int v = 0; v < NV; ++v)
-            buf_st_coherent(tmp[i][v], Vres, doff[v] + (uint32_t)(cb + i) * rowbytes);
+          st_row<NV, kCoherent>(tmp[i], Vres, doff + (uint32_t)(cb + i) * rowbytes, 0);
       }
     }
     // a launch of one stratum is ordered by the kernel boundary instead;
@@ -359,42 +403,230 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
   }
 }
 
+// Variant with V left in global memory, for column slices too wide to stage
+// in LDS next to one wave per row-block (or blocks with far fewer ratings
+// than columns, where staging the whole slice would dominate).
+//
+// Each rating's v row is prefetched D ratings ahead into a second register
+// ring, like the u rows.  That prefetch misses the updates made to the same
+// column by the D - 1 ratings in between.  The decoded window therefore
+// starts one chunk early (lane L holds rating c - CH + L), so at every step
+// the columns of the previous D - 1 ratings are in the wave: one compare
+// across the lanes finds the most recent of them with the next rating's
+// column, and its updated row is read back from a per-wave LDS ring that
+// keeps the result of each of the last D steps (slot = rating mod D).  The
+// previous step's result is forwarded in registers.
+//
+// COH: V is accessed with device-scope (sc1) loads and stores, for the
+// persistent schedule, where a column-block moves between waves (and XCDs)
+// inside one launch; a launch of one stratum touches every column from one
+// wave only and uses plain cached accesses.
+template <int KP, bool MASK, bool COH>
+__global__ void __launch_bounds__(256) k_sgd_gv(SgdParams P) {
+  using L = Lanes<KP, MASK>;
+  constexpr int NV = L::NV;
+  constexpr int KPL = L::KPL;
+  constexpr int D = kPrefetch;
+  constexpr int CH = D;
+  static_assert(D == 16, "the window holds the previous chunk, the current one and the next two");
+  constexpr int VPOL = COH ? kCoherent : 0;
+  constexpr uint32_t kNoCol = 0xFFFFFFFFu;  // column of ratings before the block: matches none
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int b = row_block_of_wave(P, wave);
+  if (b >= P.p) return;
+  const L ln(P.k);
+  const int lane = ln.lane;
+  const uint32_t doff = ln.doff;
+
+  extern __shared__ float lds[];
+  const Grid G{P.n, P.m, P.p};
+  const int k = P.k;
+  const uint32_t rowbytes = (uint32_t)k * 4u;
+  const uint32_t slotbytes = (uint32_t)KP * 4u;
+
+  const int64_t r0 = G.row_start(b);
+  const uint32_t rows_b = (uint32_t)(G.row_start(b + 1) - r0);
+  const __amdgpu_buffer_rsrc_t Ures =
+      __builtin_amdgcn_make_buffer_rsrc(P.U + r0 * k, (short)0, (int)(rows_b * rowbytes), kBufWord3);
+  // this wave's ring of the last D results (D slots of KP floats)
+  const uint32_t rbase = ((uint32_t)wave * D * KP + ln.first) * 4u;
+  char *ldsb = reinterpret_cast<char *>(lds);
+  const int64_t *blk_b = P.blk + (int64_t)b * P.stride_b;
+  float alpha;
+  asm("v_mov_b32 %0, %1" : "=v"(alpha) : "s"(P.alpha));
+  const float shrink = 1.0f - P.alpha * P.beta;
+  const float xscale = 1.0f / (float)KPL;
+
+  for (int s = P.s_begin; s < P.s_end; ++s) {
+    const int64_t g = P.g_base + s;
+    const int C = (b + s) % P.p;
+    const int64_t c0 = G.col_start(C);
+    const int ncols = (int)(G.col_start(C + 1) - c0);
+    const int64_t *bx = blk_b + (int64_t)s * P.stride_s;
+    const int64_t beg = uniform64(bx[0]);
+    const int32_t len = (int32_t)(uniform64(bx[1]) - beg);
+    const uint2 *rp = P.rec + (beg - P.rec_origin);
+
+    // Decoded window of chunk c: lane L holds rating t = c - CH + L.
+    //   wrow = byte offset of the row in U (0 outside the block)
+    //   wcol = byte offset of the column in the slice of V (0 past the end,
+    //          kNoCol before the start)
+    //   wx   = x / KPL
+    uint32_t wrow = 0u, wcol = 0u;
+    float wx = 0.0f;
+    auto decode = [&](uint2 w, int32_t c) {
+      const int32_t t = c - CH + lane;
+      const bool ok = t >= 0 && t < len;
+      wrow = ok ? (w.x & kRowMask) * rowbytes : 0u;
+      wcol = ok ? ((w.x >> kColShift) & kColMask) * rowbytes : (t < 0 ? kNoCol : 0u);
+      wx = __uint_as_float(w.y) * xscale;
+    };
+
+    float ring[D][NV], vring[D][NV];
+    uint32_t ringrow[D];
+    uint2 Wn1 = make_uint2(0u, 0u);
+    if (len > 0) {
+      decode(rp[lane >= CH ? lane - CH : 0], 0);
+      Wn1 = rp[lane];  // window of chunk CH
+#pragma unroll
+      for (int j = 0; j < D; ++j) {
+        ringrow[j] = rl(wrow, CH + j);
+        ld_row<NV, 0>(ring[j], Ures, doff, ringrow[j]);
+      }
+    }
+    if (s > P.s_begin) {
+      const int nb = (b + 1 == P.p) ? 0 : b + 1;
+      if (!wait_progress(P.flags + (int64_t)nb * kFlagStride, g, P.wait_ticks)) {
+        __hip_atomic_store(P.err, kErrTimeout, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        return;
+      }
+    }
+    if (len > 0) {
+      const __amdgpu_buffer_rsrc_t Vres = __builtin_amdgcn_make_buffer_rsrc(
+          P.V + c0 * k, (short)0, (int)((uint32_t)ncols * rowbytes), kBufWord3);
+#pragma unroll
+      for (int j = 0; j < D; ++j) ld_row<NV, VPOL>(vring[j], Vres, doff, rl(wcol, CH + j));
+      uint32_t prev_row = 0xFFFFFFFFu;
+      float uprev[NV], vnext[NV];
+      __builtin_amdgcn_s_waitcnt(0x0F70);
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        uprev[v] = 0.0f;
+        vnext[v] = vring[0][v];
+      }
+
+      auto chunk = [&](auto tail_tag, int32_t c) {
+        constexpr bool TAIL = decltype(tail_tag)::value;
+        // window of chunk c + 2 CH (ratings c + CH .. c + CH + 63)
+        const uint2 Wn2 = rp[c + CH + lane];
+        uint32_t ccur = rl(wcol, CH);
+#pragma unroll
+        for (int j = 0; j < CH; ++j) {
+          const float x64 = __uint_as_float(rl(__float_as_uint(wx), CH + j));
+          const uint32_t row = ringrow[j];
+          const uint32_t col1 = rl(wcol, CH + j + 1);
+          const bool same_row = row == prev_row;
+          // latest of ratings t-14 .. t-1 (lanes j+2 .. j+15) with the next
+          // rating's column: its result is in LDS slot (lane mod D)
+          // (lanes below 32, so the low half of the ballot suffices)
+          const uint32_t kMask = ((1u << (D - 2)) - 1u) << (j + 2);  // folded: j is unrolled
+          const uint32_t hit = (uint32_t)__builtin_amdgcn_ballot_w64(wcol == col1) & kMask;
+          // hit bits are >= 2, so "| 1" leaves the top bit alone and gives
+          // slot 0 (a read whose value is not used) when there is no hit
+          const uint32_t hslot = (uint32_t)(31 - __builtin_clz(hit | 1u)) & (D - 1);
+          float u[NV], vv[NV], vl[NV];
+#pragma unroll
+          for (int v = 0; v < NV; ++v) {
+            u[v] = same_row ? uprev[v] : ring[j][v];
+            vv[v] = vnext[v];
+          }
+          lds_ld<NV>(vl, ldsb, rbase + hslot * slotbytes);
+          float tpart = fmaf(-u[0], vv[0], x64);
+#pragma unroll
+          for (int v = 1; v < NV; ++v) tpart = fmaf(-u[v], vv[v], tpart);
+          const float ae = alpha * lane_total<KPL>(tpart);
+          float nu[NV], nv[NV];
+#pragma unroll
+          for (int v = 0; v < NV; ++v) {
+            nu[v] = fmaf(ae, vv[v], shrink * u[v]);
+            nv[v] = fmaf(ae, u[v], shrink * vv[v]);
+          }
+          lds_st<NV>(nv, ldsb, rbase + (uint32_t)j * slotbytes);
+          if constexpr (TAIL) {
+            const bool real = c + j < len;
+            st_row<NV, 0>(nu, Ures, doff + (real ? row : kOff), 0);
+            st_row<NV, VPOL>(nv, Vres, doff + (real ? ccur : kOff), 0);
+          } else {
+            st_row<NV, 0>(nu, Ures, doff, row);
+            st_row<NV, VPOL>(nv, Vres, doff, ccur);
+          }
+#pragma unroll
+          for (int v = 0; v < NV; ++v) {
+            uprev[v] = nu[v];
+            vnext[v] = (col1 == ccur) ? nv[v] : (hit ? vl[v] : vring[(j + 1) % D][v]);
+          }
+          prev_row = row;
+          ccur = col1;
+          // prefetch u and v of rating t + D (lane j + 2 CH) into slot j
+          ringrow[j] = rl(wrow, 2 * CH + j);
+          ld_row<NV, 0>(ring[j], Ures, doff, ringrow[j]);
+          ld_row<NV, VPOL>(vring[j], Vres, doff, rl(wcol, 2 * CH + j));
+        }
+        decode(Wn1, c + CH);
+        Wn1 = Wn2;
+      };
+      const int32_t full = len & ~(CH - 1);
+      for (int32_t c = 0; c < full; c += CH) chunk(std::false_type{}, c);
+      if (full < len) chunk(std::true_type{}, full);
+    }
+    if (P.s_end - P.s_begin > 1) publish_progress(P.flags + (int64_t)b * kFlagStride, g + 1);
+  }
+}
+
 template <int KP>
-const void *kernel_for(bool mask) {
+const void *kernel_for(bool mask, int vmode) {
+  if (vmode == kVGlobalCoherent)
+    return mask ? reinterpret_cast<const void *>(&k_sgd_gv<KP, true, true>)
+                : reinterpret_cast<const void *>(&k_sgd_gv<KP, false, true>);
+  if (vmode == kVGlobal)
+    return mask ? reinterpret_cast<const void *>(&k_sgd_gv<KP, true, false>)
+                : reinterpret_cast<const void *>(&k_sgd_gv<KP, false, false>);
   return mask ? reinterpret_cast<const void *>(&k_sgd_lds<KP, true>)
               : reinterpret_cast<const void *>(&k_sgd_lds<KP, false>);
 }
 
-const void *sgd_kernel(int kp, bool mask) {
+const void *sgd_kernel(int kp, bool mask, int vmode) {
   switch (kp) {
-    case 16: return kernel_for<16>(mask);
-    case 32: return kernel_for<32>(mask);
-    case 64: return kernel_for<64>(mask);
-    case 128: return kernel_for<128>(mask);
-    case 256: return kernel_for<256>(mask);
+    case 16: return kernel_for<16>(mask, vmode);
+    case 32: return kernel_for<32>(mask, vmode);
+    case 64: return kernel_for<64>(mask, vmode);
+    case 128: return kernel_for<128>(mask, vmode);
+    case 256: return kernel_for<256>(mask, vmode);
     default: return nullptr;
   }
 }
 
 }  // namespace
 
-hipError_t sgd_set_lds_limit(int kp, bool mask, size_t lds_bytes) {
-  const void *f = sgd_kernel(kp, mask);
+size_t sgd_gv_lds_per_wave(int kp) { return (size_t)kPrefetch * kp * sizeof(float); }
+
+hipError_t sgd_set_lds_limit(int kp, bool mask, int vmode, size_t lds_bytes) {
+  const void *f = sgd_kernel(kp, mask, vmode);
   if (!f) return hipErrorInvalidValue;
   return hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
 }
 
-hipError_t sgd_occupancy(int kp, bool mask, int waves_per_group, size_t lds_bytes,
+hipError_t sgd_occupancy(int kp, bool mask, int vmode, int waves_per_group, size_t lds_bytes,
                          int *groups_per_cu) {
-  const void *f = sgd_kernel(kp, mask);
+  const void *f = sgd_kernel(kp, mask, vmode);
   if (!f) return hipErrorInvalidValue;
   return hipOccupancyMaxActiveBlocksPerMultiprocessor(groups_per_cu, f, 64 * waves_per_group,
                                                       lds_bytes);
 }
 
-hipError_t launch_sgd(const SgdParams &P, int kp, int waves_per_group, bool cooperative,
+hipError_t launch_sgd(const SgdParams &P, int kp, int vmode, int waves_per_group, bool cooperative,
                       size_t lds_bytes, hipStream_t stream) {
-  const void *f = sgd_kernel(kp, P.k != kp);
+  const void *f = sgd_kernel(kp, P.k != kp, vmode);
   if (!f) return hipErrorInvalidValue;
   const unsigned groups = (unsigned)((P.p + waves_per_group - 1) / waves_per_group);
   const unsigned threads = 64u * (unsigned)waves_per_group;

@@ -14,21 +14,23 @@ pytestmark = pytest.mark.gpu
 TOL = 1e-4
 
 
-def _run(w, epochs, budget=0, schedule=0):
+def _run(w, epochs, budget=0, schedule=0, v_staging=0):
     from paper_2304_13724_amd import bgmf
     with bgmf.Model(w.n, w.m, w.k, w.p) as mdl:
         mdl.set_option(bgmf.BGMF_OPT_RATINGS_BUDGET, budget)
         mdl.set_option(bgmf.BGMF_OPT_SCHEDULE, schedule)
+        mdl.set_option(bgmf.BGMF_OPT_V_STAGING, v_staging)
         mdl.set_factors(w.U0, w.V0)
         mdl.load_coo(w.rows, w.cols, w.vals)
         slots = mdl.get_option(bgmf.BGMF_OPT_STREAM_SLOTS)
+        chunks = mdl.get_option(bgmf.BGMF_OPT_STREAM_CHUNKS)
         bp, perm = mdl.get_layout()
         hist = []
         for _ in range(epochs):
             mdl.epoch(w.alpha, w.beta)
             hist.append(mdl.rmse())
         U, V = mdl.get_factors()
-    return U, V, hist, bp, perm, slots
+    return U, V, hist, bp, perm, slots, chunks
 
 
 def _stratum_bytes(w):
@@ -48,23 +50,45 @@ CASES = {
 
 
 @pytest.mark.parametrize("case", sorted(CASES))
-@pytest.mark.parametrize("nslots", [2, 3, 7])
-def test_ooc_bit_identical_to_incore(case, nslots):
+@pytest.mark.parametrize("strata", [2, 3, 7, "half"])
+def test_ooc_bit_identical_to_incore(case, strata):
+    """A budget of ``strata`` times the widest stratum (or of half the
+    ratings): 2 ring slots below 3, else 3, each taking a chunk of as many
+    consecutive strata as fit."""
     w = CASES[case]()
-    budget = nslots * _stratum_bytes(w) + 100
+    if strata == "half":
+        budget = w.nnz * 8 // 2
+        strata = budget // _stratum_bytes(w)
+    else:
+        budget = strata * _stratum_bytes(w) + 100
     inc = _run(w, 3)
     ooc = _run(w, 3, budget=budget)
-    assert inc[5] == 0 and ooc[5] == nslots
+    assert inc[5] == 0 and inc[6] == 0
+    assert ooc[5] == (2 if strata < 3 else 3)
+    assert 1 <= ooc[6] <= w.p
+    if strata >= 7:
+        assert ooc[6] < w.p  # several strata per chunk
     assert np.array_equal(ooc[0], inc[0]) and np.array_equal(ooc[1], inc[1])
     assert np.array_equal(ooc[3], inc[3]) and np.array_equal(ooc[4], inc[4])
     for a, b in zip(ooc[2], inc[2]):
         assert abs(a - b) <= 1e-12 * b
 
 
+@pytest.mark.parametrize("schedule,v_staging", [(1, 0), (0, 2), (2, 2), (2, 1)])
+def test_ooc_schedules_and_placements(schedule, v_staging):
+    """Chunks swept one launch per stratum, with V in global memory, or
+    with a persistent launch per chunk: all equal the in-core sweep."""
+    w = CASES["large_shape"]()
+    inc = _run(w, 2)
+    ooc = _run(w, 2, budget=20 * _stratum_bytes(w), schedule=schedule, v_staging=v_staging)
+    assert ooc[5] == 3 and ooc[6] < w.p
+    assert np.array_equal(ooc[0], inc[0]) and np.array_equal(ooc[1], inc[1])
+
+
 def test_ooc_matches_oracle():
     w = CASES["large_shape"]()
     U_ref, V_ref, hist_ref, bp_ref, perm_ref = oracle_run(w, 2)
-    U, V, hist, bp, perm, slots = _run(w, 2, budget=2 * _stratum_bytes(w))
+    U, V, hist, bp, perm, slots, _ = _run(w, 2, budget=2 * _stratum_bytes(w))
     assert slots == 2
     assert np.array_equal(bp, bp_ref) and np.array_equal(perm, perm_ref)
     assert row_rel_err(U, U_ref) <= 2 * TOL and row_rel_err(V, V_ref) <= 2 * TOL
