@@ -146,17 +146,20 @@ int bgmf_factor_ptrs(bgmf_t *h, float **U_dev, float **V_dev);
 #define BGMF_OPT_RATINGS_BUDGET 4 /* device bytes the bucketed ratings may occupy
                                     during epochs; 0 (default) = no limit.  Takes
                                     effect at the next bgmf_load_coo.  If the
-                                    ratings (8 bytes each) do not fit, they are
-                                    kept in pinned host memory in stratum order
-                                    and streamed through a ring of 3 (else 2)
-                                    device slots that split the budget; each slot
-                                    takes a chunk of consecutive strata, copied on
-                                    a side stream while the previous chunk is
-                                    swept.  A slot must hold the widest stratum
-                                    plus 256 records (else BGMF_E_BUDGET); U and V
-                                    stay resident.  This applies the paper's point
-                                    that a block-based sweep only needs the blocks
-                                    in flight on the device (Sections 1.2 and 2.2).
+                                    ratings (8 bytes each, plus 256 records of
+                                    padding) do not fit, they are kept in pinned
+                                    host memory in stratum order.  The budget is
+                                    then split into a ring of 3 (else 2) device
+                                    slots and a resident region: the first strata
+                                    of the epoch stay resident (copied once, at
+                                    load), the others stream through the ring in
+                                    chunks of consecutive strata, each copied on a
+                                    side stream while earlier strata are swept.  A
+                                    slot must hold the widest stratum plus 256
+                                    records (else BGMF_E_BUDGET); U and V stay
+                                    resident.  This applies the paper's point that
+                                    a block-based sweep only needs the blocks in
+                                    flight on the device (Sections 1.2 and 2.2).
                                     Results are bit-identical to the in-core sweep. */
 #define BGMF_OPT_STREAM_SLOTS  5 /* read-only: number of ring slots when the
                                     loaded ratings stream from host memory, else 0 */
@@ -174,6 +177,8 @@ int bgmf_factor_ptrs(bgmf_t *h, float **U_dev, float **V_dev);
                                     stratum) */
 #define BGMF_OPT_STREAM_CHUNKS 8 /* read-only: chunks of strata streamed per epoch
                                     when the ratings stream from host memory, else 0 */
+#define BGMF_OPT_RESIDENT_STRATA 9 /* read-only: strata whose ratings stay on the
+                                    device (all p unless they stream) */
 int bgmf_set_option(bgmf_t *h, int32_t option, int64_t value);
 int bgmf_get_option(const bgmf_t *h, int32_t option, int64_t *value);
 

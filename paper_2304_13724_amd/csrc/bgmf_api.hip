@@ -54,11 +54,14 @@ struct bgmf {
   bool ooc = false;
   uint2 *host_rec = nullptr;     // stratum-major records (pinned)
   int32_t *host_perm = nullptr;  // slot-order input positions (pinned)
+  uint2 *resident = nullptr;     // strata [0, s_res), copied once per load
+  int32_t s_res = 0;
   uint2 *ring = nullptr;         // device slots of slot_recs records each
   int nslots = 0;
   int64_t slot_recs = 0;
   std::vector<int64_t> strat;    // p + 1 record offsets of the strata
   std::vector<int32_t> chunk;    // chunk c = strata [chunk[c], chunk[c + 1]), one slot each
+  size_t issued = 0;             // chunks whose copy has been queued in the current pass
   hipStream_t side = nullptr;    // copies into the ring
   std::vector<hipEvent_t> ready, freed;
   std::vector<bool> slot_used;
@@ -94,6 +97,7 @@ void free_layout(bgmf_t *h) {
   hipFree(h->perm);
   hipFree(h->rec);
   hipFree(h->ring);
+  hipFree(h->resident);
   if (h->host_rec) hipHostFree(h->host_rec);
   if (h->host_perm) hipHostFree(h->host_perm);
   for (auto ev : h->ready) hipEventDestroy(ev);
@@ -104,7 +108,8 @@ void free_layout(bgmf_t *h) {
   h->chunk.clear();
   h->block_ptr = h->wblock_ptr = nullptr;
   h->perm = nullptr;
-  h->rec = h->ring = h->host_rec = nullptr;
+  h->rec = h->ring = h->host_rec = h->resident = nullptr;
+  h->s_res = 0;
   h->host_perm = nullptr;
   h->nslots = 0;
   h->ooc = false;
@@ -398,19 +403,26 @@ int bgmf_load_coo(bgmf_t *h, const int32_t *rows, const int32_t *cols, const flo
     int64_t widest = 0;
     for (int64_t s2 = 0; s2 <= h->p; ++s2) h->strat[s2] = bp[s2 * h->p];
     for (int64_t s2 = 0; s2 < h->p; ++s2) widest = std::max(widest, h->strat[s2 + 1] - h->strat[s2]);
-    // Three slots (copy ahead, compute, drain) if the budget holds three of
-    // the widest stratum, else two; each slot takes a chunk of consecutive
-    // strata, as many as fit, so that one copy and one launch cover many
-    // strata.
+    // The budget is split into a ring of 3 (else 2) slots and a resident
+    // region.  A slot holds the widest stratum plus the padding, and is made
+    // a quarter of the budget when that fits: each chunk of strata in a slot
+    // costs one copy and, with the persistent schedule, one launch, whose
+    // end is a barrier across all row-blocks, so few large chunks are
+    // better.  The resident region keeps the first strata of the epoch on
+    // the device for good; the ring streams the others, and their first
+    // copies run while the resident strata are swept.
     const int64_t need = widest + kRecPad;
+    const int64_t budget_recs = h->budget / (int64_t)sizeof(uint2);
     h->nslots = 0;
     for (int cand : {3, 2}) {
-      const int64_t cap = h->budget / ((int64_t)cand * (int64_t)sizeof(uint2));
-      if (cap >= need) {
-        h->nslots = cand;
-        h->slot_recs = cap;
-        break;
+      for (int64_t slot : {std::max(need, budget_recs / 4), need}) {
+        if ((int64_t)cand * slot <= budget_recs) {
+          h->nslots = cand;
+          h->slot_recs = slot;
+          break;
+        }
       }
+      if (h->nslots) break;
     }
     if (h->nslots == 0) {
       const int64_t slot_bytes = need * (int64_t)sizeof(uint2);
@@ -420,11 +432,15 @@ int bgmf_load_coo(bgmf_t *h, const int32_t *rows, const int32_t *cols, const flo
                   "needs %lld bytes)",
                   (long long)h->budget, (long long)slot_bytes);
     }
-    h->chunk.assign(1, 0);
-    for (int32_t s2 = 0; s2 < h->p; ++s2)
+    const int64_t res_cap = budget_recs - (int64_t)h->nslots * h->slot_recs;
+    h->s_res = 0;
+    while (h->s_res < h->p && h->strat[h->s_res + 1] + kRecPad <= res_cap) ++h->s_res;
+    // chunks of consecutive streamed strata, each as many as fit in a slot
+    h->chunk.assign(1, h->s_res);
+    for (int32_t s2 = h->s_res; s2 < h->p; ++s2)
       if (h->strat[s2 + 1] - h->strat[h->chunk.back()] + kRecPad > h->slot_recs)
         h->chunk.push_back(s2);
-    h->chunk.push_back(h->p);
+    if (h->chunk.back() != h->p) h->chunk.push_back(h->p);
     const int64_t slot_bytes = h->slot_recs * (int64_t)sizeof(uint2);
     if (!h->side) HIP_TRY(h, hipStreamCreateWithFlags(&h->side, hipStreamNonBlocking));
     HIP_TRY(h, hipHostMalloc(reinterpret_cast<void **>(&h->host_rec),
@@ -438,6 +454,13 @@ int bgmf_load_coo(bgmf_t *h, const int32_t *rows, const int32_t *cols, const flo
     hipFree(h->perm);
     h->rec = nullptr;
     h->perm = nullptr;
+    if (h->s_res > 0) {
+      const int64_t count = h->strat[h->s_res];
+      HIP_TRY(h, hipMalloc(&h->resident, (size_t)(count + kRecPad) * sizeof(uint2)));
+      HIP_TRY(h, hipMemcpy(h->resident, h->host_rec, (size_t)count * sizeof(uint2),
+                           hipMemcpyHostToDevice));
+      HIP_TRY(h, hipMemset(h->resident + count, 0, (size_t)kRecPad * sizeof(uint2)));
+    }
     HIP_TRY(h, hipMalloc(&h->ring, (size_t)h->nslots * (size_t)slot_bytes));
     HIP_TRY(h, hipMemset(h->ring, 0, (size_t)h->nslots * (size_t)slot_bytes));
     h->ready.assign(h->nslots, nullptr);
@@ -460,28 +483,52 @@ int bgmf_load_coo(bgmf_t *h, const int32_t *rows, const int32_t *cols, const flo
 
 namespace {
 
-// Out-of-core streaming of chunk c (consecutive strata) into its ring slot
-// on the side stream; returns the slot's device records.  The copy waits
-// until the kernels that last read the slot have finished, and the caller's
-// stream waits for the copy.
-int stage_chunk(bgmf_t *h, size_t c, const uint2 **slot_rec) {
+// Out-of-core streaming, one pass over the strata (an epoch or an RMSE
+// pass).  Chunk c goes to ring slot c mod nslots.  Its copy runs on the side
+// stream once the kernels that last read the slot have finished (the slot's
+// freed event); the handle's stream waits for the copy (ready event) just
+// before the chunk's kernels, and records freed after them.  The copies of
+// the first nslots chunks are queued at the start of the pass, so they run
+// while the resident strata are swept.
+int queue_copy(bgmf_t *h, size_t c) {
   const int slot = (int)(c % (size_t)h->nslots);
   uint2 *dst = h->ring + (size_t)slot * (size_t)h->slot_recs;
   const int64_t first = h->strat[h->chunk[c]];
   const int64_t count = h->strat[h->chunk[c + 1]] - first;
   if (h->slot_used[slot]) HIP_TRY(h, hipStreamWaitEvent(h->side, h->freed[slot], 0));
-  HIP_TRY(h, hipMemcpyAsync(dst, h->host_rec + first, (size_t)count * sizeof(uint2),
-                            hipMemcpyHostToDevice, h->side));
+  if (count > 0)
+    HIP_TRY(h, hipMemcpyAsync(dst, h->host_rec + first, (size_t)count * sizeof(uint2),
+                              hipMemcpyHostToDevice, h->side));
   HIP_TRY(h, hipEventRecord(h->ready[slot], h->side));
-  HIP_TRY(h, hipStreamWaitEvent(h->stream, h->ready[slot], 0));
-  *slot_rec = dst;
   return BGMF_OK;
 }
 
-int release_slot(bgmf_t *h, size_t c) {
+int stream_begin(bgmf_t *h) {
+  const size_t nch = h->chunk.size() - 1;
+  for (h->issued = 0; h->issued < std::min(nch, (size_t)h->nslots); ++h->issued) {
+    int rc = queue_copy(h, h->issued);
+    if (rc != BGMF_OK) return rc;
+  }
+  return BGMF_OK;
+}
+
+// Make the handle's stream wait for chunk c; returns its device records.
+int chunk_ready(bgmf_t *h, size_t c, const uint2 **slot_rec) {
+  const int slot = (int)(c % (size_t)h->nslots);
+  HIP_TRY(h, hipStreamWaitEvent(h->stream, h->ready[slot], 0));
+  *slot_rec = h->ring + (size_t)slot * (size_t)h->slot_recs;
+  return BGMF_OK;
+}
+
+// The kernels of chunk c are queued: free its slot and queue the next copy.
+int chunk_done(bgmf_t *h, size_t c) {
   const int slot = (int)(c % (size_t)h->nslots);
   HIP_TRY(h, hipEventRecord(h->freed[slot], h->stream));
   h->slot_used[slot] = true;
+  if (h->issued < h->chunk.size() - 1) {
+    int rc = queue_copy(h, h->issued++);
+    if (rc != BGMF_OK) return rc;
+  }
   return BGMF_OK;
 }
 
@@ -540,35 +587,40 @@ int bgmf_epoch(bgmf_t *h, float alpha, float beta) {
   const SweepShape sh = sweep_shape(h);
   HIP_TRY(h, hipEventRecord(h->ev[0], h->stream));
   if (h->ooc) {
-    // per chunk of strata in a ring slot: one persistent launch, or one
-    // launch per stratum
+    // resident strata, then the streamed chunks; each range is one
+    // persistent launch or one launch per stratum
     P.blk = h->block_ptr;  // stratum-major: block (b, s) at s*p + b
     P.stride_b = 1;
     P.stride_s = h->p;
-    for (size_t c = 0; c + 1 < h->chunk.size(); ++c) {
-      const int32_t s0 = h->chunk[c], s1 = h->chunk[c + 1];
-      if (h->strat[s1] == h->strat[s0]) continue;  // no ratings in these strata
-      const uint2 *slot_rec = nullptr;
-      int rc = stage_chunk(h, c, &slot_rec);
-      if (rc != BGMF_OK) return rc;
-      P.rec = slot_rec;
-      P.rec_origin = h->strat[s0];
+    auto sweep_range = [&](const uint2 *rec, int64_t origin, int32_t s0, int32_t s1) -> int {
+      P.rec = rec;
+      P.rec_origin = origin;
       if (sh.persistent && s1 - s0 > 1) {
         P.s_begin = s0;
         P.s_end = s1;
         HIP_TRY(h, launch_sgd(P, h->kp, sh.vmode, sh.wpg, true, sh.lds_bytes, h->stream));
-      } else {
-        const int vmode = sh.lds ? kVLds : kVGlobal;
-        for (int32_t s2 = s0; s2 < s1; ++s2) {
-          if (h->strat[s2 + 1] == h->strat[s2]) continue;
-          P.s_begin = s2;
-          P.s_end = s2 + 1;
-          HIP_TRY(h, launch_sgd(P, h->kp, vmode, sh.wpg, false, sh.lds_bytes, h->stream));
-        }
+        return BGMF_OK;
       }
-      rc = release_slot(h, c);
-      if (rc != BGMF_OK) return rc;
+      const int vmode = sh.lds ? kVLds : kVGlobal;
+      for (int32_t s2 = s0; s2 < s1; ++s2) {
+        if (h->strat[s2 + 1] == h->strat[s2]) continue;
+        P.s_begin = s2;
+        P.s_end = s2 + 1;
+        HIP_TRY(h, launch_sgd(P, h->kp, vmode, sh.wpg, false, sh.lds_bytes, h->stream));
+      }
+      return BGMF_OK;
+    };
+    int rc = stream_begin(h);
+    if (rc == BGMF_OK && h->s_res > 0) rc = sweep_range(h->resident, 0, 0, h->s_res);
+    for (size_t c = 0; rc == BGMF_OK && c + 1 < h->chunk.size(); ++c) {
+      const int32_t s0 = h->chunk[c], s1 = h->chunk[c + 1];
+      const uint2 *slot_rec = nullptr;
+      rc = chunk_ready(h, c, &slot_rec);
+      if (rc == BGMF_OK && h->strat[s1] > h->strat[s0])
+        rc = sweep_range(slot_rec, h->strat[s0], s0, s1);
+      if (rc == BGMF_OK) rc = chunk_done(h, c);
     }
+    if (rc != BGMF_OK) return rc;
   } else if (sh.persistent) {
     P.s_begin = 0;
     P.s_end = h->p;
@@ -594,15 +646,20 @@ int bgmf_rmse(bgmf_t *h, double *out) {
   HIP_TRY(h, hipEventRecord(h->ev[2], h->stream));
   if (h->ooc) {
     HIP_TRY(h, rmse_stratum_begin(h->partials, h->p, h->stream));
+    int rc = stream_begin(h);
+    if (rc != BGMF_OK) return rc;
+    if (h->s_res > 0)
+      HIP_TRY(h, rmse_stratum_add(h->resident, 0, h->block_ptr, 0, h->s_res, h->U, h->V, h->n,
+                                  h->m, h->k, h->p, h->partials, h->stream));
     for (size_t c = 0; c + 1 < h->chunk.size(); ++c) {
       const int32_t s0 = h->chunk[c], s1 = h->chunk[c + 1];
-      if (h->strat[s1] == h->strat[s0]) continue;
       const uint2 *slot_rec = nullptr;
-      int rc = stage_chunk(h, c, &slot_rec);
+      rc = chunk_ready(h, c, &slot_rec);
       if (rc != BGMF_OK) return rc;
-      HIP_TRY(h, rmse_stratum_add(slot_rec, h->strat[s0], h->block_ptr, s0, s1, h->U, h->V, h->n,
-                                  h->m, h->k, h->p, h->partials, h->stream));
-      rc = release_slot(h, c);
+      if (h->strat[s1] > h->strat[s0])
+        HIP_TRY(h, rmse_stratum_add(slot_rec, h->strat[s0], h->block_ptr, s0, s1, h->U, h->V,
+                                    h->n, h->m, h->k, h->p, h->partials, h->stream));
+      rc = chunk_done(h, c);
       if (rc != BGMF_OK) return rc;
     }
     HIP_TRY(h, rmse_stratum_end(h->partials, h->p, h->nnz, h->d_rmse, h->stream));
@@ -691,6 +748,8 @@ int bgmf_set_option(bgmf_t *h, int32_t option, int64_t value) {
       return fail(h, BGMF_E_ARG, "BGMF_OPT_PLACEMENT is read-only");
     case BGMF_OPT_STREAM_CHUNKS:
       return fail(h, BGMF_E_ARG, "BGMF_OPT_STREAM_CHUNKS is read-only");
+    case BGMF_OPT_RESIDENT_STRATA:
+      return fail(h, BGMF_E_ARG, "BGMF_OPT_RESIDENT_STRATA is read-only");
     default:
       return fail(h, BGMF_E_ARG, "unknown option %d", option);
   }
@@ -708,6 +767,7 @@ int bgmf_get_option(const bgmf_t *h, int32_t option, int64_t *value) {
     case BGMF_OPT_STREAM_CHUNKS:
       *value = h->ooc ? (int64_t)h->chunk.size() - 1 : 0;
       return BGMF_OK;
+    case BGMF_OPT_RESIDENT_STRATA: *value = h->ooc ? h->s_res : h->p; return BGMF_OK;
     case BGMF_OPT_PLACEMENT: {
       const SweepShape sh = sweep_shape(h);
       *value = (sh.lds ? 1 : 2) | (sh.persistent ? 4 : 0);

@@ -24,13 +24,14 @@ def _run(w, epochs, budget=0, schedule=0, v_staging=0):
         mdl.load_coo(w.rows, w.cols, w.vals)
         slots = mdl.get_option(bgmf.BGMF_OPT_STREAM_SLOTS)
         chunks = mdl.get_option(bgmf.BGMF_OPT_STREAM_CHUNKS)
+        resident = mdl.get_option(bgmf.BGMF_OPT_RESIDENT_STRATA)
         bp, perm = mdl.get_layout()
         hist = []
         for _ in range(epochs):
             mdl.epoch(w.alpha, w.beta)
             hist.append(mdl.rmse())
         U, V = mdl.get_factors()
-    return U, V, hist, bp, perm, slots, chunks
+    return U, V, hist, bp, perm, slots, chunks, resident
 
 
 def _stratum_bytes(w):
@@ -56,7 +57,8 @@ def test_ooc_bit_identical_to_incore(case, strata):
     ratings): 2 ring slots below 3, else 3, each taking a chunk of as many
     consecutive strata as fit."""
     w = CASES[case]()
-    if strata == "half":
+    half = strata == "half"
+    if half:
         budget = w.nnz * 8 // 2
         strata = budget // _stratum_bytes(w)
     else:
@@ -65,9 +67,12 @@ def test_ooc_bit_identical_to_incore(case, strata):
     ooc = _run(w, 3, budget=budget)
     assert inc[5] == 0 and inc[6] == 0
     assert ooc[5] == (2 if strata < 3 else 3)
-    assert 1 <= ooc[6] <= w.p
+    assert inc[7] == w.p and 0 <= ooc[7] < w.p
+    assert 1 <= ooc[6] <= w.p - ooc[7]
     if strata >= 7:
-        assert ooc[6] < w.p  # several strata per chunk
+        assert ooc[7] > 0  # the budget beyond the ring keeps strata resident
+    if half:
+        assert ooc[6] < w.p - ooc[7]  # slots of a quarter of the budget: several strata each
     assert np.array_equal(ooc[0], inc[0]) and np.array_equal(ooc[1], inc[1])
     assert np.array_equal(ooc[3], inc[3]) and np.array_equal(ooc[4], inc[4])
     for a, b in zip(ooc[2], inc[2]):
@@ -81,14 +86,14 @@ def test_ooc_schedules_and_placements(schedule, v_staging):
     w = CASES["large_shape"]()
     inc = _run(w, 2)
     ooc = _run(w, 2, budget=20 * _stratum_bytes(w), schedule=schedule, v_staging=v_staging)
-    assert ooc[5] == 3 and ooc[6] < w.p
+    assert ooc[5] == 3 and ooc[6] < w.p and ooc[7] > 0
     assert np.array_equal(ooc[0], inc[0]) and np.array_equal(ooc[1], inc[1])
 
 
 def test_ooc_matches_oracle():
     w = CASES["large_shape"]()
     U_ref, V_ref, hist_ref, bp_ref, perm_ref = oracle_run(w, 2)
-    U, V, hist, bp, perm, slots, _ = _run(w, 2, budget=2 * _stratum_bytes(w))
+    U, V, hist, bp, perm, slots, _, _ = _run(w, 2, budget=2 * _stratum_bytes(w))
     assert slots == 2
     assert np.array_equal(bp, bp_ref) and np.array_equal(perm, perm_ref)
     assert row_rel_err(U, U_ref) <= 2 * TOL and row_rel_err(V, V_ref) <= 2 * TOL
