@@ -16,6 +16,9 @@ Functions follow the paper's Section 1:
     Algorithm 1 with one pass per block
   * ``rmse``     — whole-matrix RMSE used by Algorithm 1's termination test
   * ``loss``     — the objective of Eq. 1 (fp64)
+  * ``sgd_update_f64`` / ``epoch_f64`` — the same step and epoch carried out
+    in binary64, the exact-arithmetic reference for measuring how far the
+    binary32 schedule (the oracle's or the GPU's) drifts through rounding
 """
 from __future__ import annotations
 
@@ -53,11 +56,14 @@ def _load():
         i32p = np.ctypeslib.ndpointer(np.int32, flags="C_CONTIGUOUS")
         i64p = np.ctypeslib.ndpointer(np.int64, flags="C_CONTIGUOUS")
         f32p = np.ctypeslib.ndpointer(np.float32, flags="C_CONTIGUOUS")
+        f64p = np.ctypeslib.ndpointer(np.float64, flags="C_CONTIGUOUS")
         I64, I32, F32, F64 = ctypes.c_int64, ctypes.c_int32, ctypes.c_float, ctypes.c_double
         lib.oracle_bucket.argtypes = [I64, I64, I64, I64, i32p, i32p, i64p, i32p]
         lib.oracle_bucket.restype = ctypes.c_int
         lib.oracle_sgd_update.argtypes = [I32, f32p, f32p, F32, F32, F32]
         lib.oracle_sgd_update.restype = None
+        lib.oracle_sgd_update_f64.argtypes = [I32, f64p, f64p, F32, F32, F32]
+        lib.oracle_sgd_update_f64.restype = None
         lib.oracle_epoch.argtypes = [I64, I32, i32p, i32p, f32p, i64p, i32p, f32p, f32p, F32, F32]
         lib.oracle_epoch.restype = None
         lib.oracle_epoch_ordered.argtypes = [I64, I32, i32p, i32p, f32p, i64p, i32p, f32p, f32p,
@@ -66,6 +72,9 @@ def _load():
         lib.oracle_epoch_mt.argtypes = [I64, I32, i32p, i32p, f32p, i64p, i32p, f32p, f32p,
                                         F32, F32, I32]
         lib.oracle_epoch_mt.restype = ctypes.c_int
+        lib.oracle_epoch_mt_f64.argtypes = [I64, I32, i32p, i32p, f32p, i64p, i32p, f64p, f64p,
+                                            F32, F32, I32]
+        lib.oracle_epoch_mt_f64.restype = ctypes.c_int
         lib.oracle_rmse.argtypes = [I32, I64, i32p, i32p, f32p, f32p, f32p]
         lib.oracle_rmse.restype = F64
         lib.oracle_loss.argtypes = [I32, I64, i32p, i32p, f32p, f32p, f32p, F64]
@@ -128,6 +137,28 @@ def epoch_mt(p, rows, cols, vals, block_ptr, perm, U, V, alpha, beta, threads):
     args = _epoch_args(p, rows, cols, vals, block_ptr, perm, U, V)
     assert args[7] is U and args[8] is V
     return int(_load().oracle_epoch_mt(*args, float(alpha), float(beta), int(threads)))
+
+
+def sgd_update_f64(u, v, x: float, alpha: float, beta: float):
+    """One step of Eq. 2-3 in binary64 on copies of u, v (x, alpha, beta
+    are rounded to binary32 first, as the GPU receives them)."""
+    u = _c(u, np.float64).copy()
+    v = _c(v, np.float64).copy()
+    _load().oracle_sgd_update_f64(u.shape[0], u, v, float(x), float(alpha), float(beta))
+    return u, v
+
+
+def epoch_f64(p, rows, cols, vals, block_ptr, perm, U64, V64, alpha, beta, threads=1):
+    """The epoch in binary64, in place on float64 U64 and V64: the same
+    schedule and operation order as ``epoch``, as an exact-arithmetic
+    reference for measuring binary32 rounding; returns threads used."""
+    args = list(_epoch_args(p, rows, cols, vals, block_ptr, perm, np.zeros((1, 1), np.float32),
+                            np.zeros((1, 1), np.float32)))
+    U64 = _c(U64, np.float64)
+    V64 = _c(V64, np.float64)
+    args[1] = int(U64.shape[1])
+    args[7], args[8] = U64, V64
+    return int(_load().oracle_epoch_mt_f64(*args, float(alpha), float(beta), int(threads)))
 
 
 def rmse(rows, cols, vals, U, V) -> float:

@@ -121,6 +121,27 @@ void oracle_sgd_update(int32_t k, float *u, float *v, float x, float alpha, floa
     sgd_step(k, u, v, x, alpha, beta);
 }
 
+/* The same step carried out in binary64 (factors held in double): the
+ * reference against which the rounding of the binary32 schedule is
+ * measured.  x, alpha and beta are the binary32 inputs, widened exactly. */
+static void sgd_step_f64(int k, double *u, double *v, double x, double alpha, double beta)
+{
+    double acc = 0.0;
+    for (int g = 0; g < k; ++g) acc = acc + u[g] * v[g];
+    double err = x - acc;
+    for (int g = 0; g < k; ++g) {
+        double uo = u[g];
+        double vo = v[g];
+        u[g] = uo + alpha * ((err * vo) - (beta * uo));
+        v[g] = vo + alpha * ((err * uo) - (beta * vo));
+    }
+}
+
+void oracle_sgd_update_f64(int32_t k, double *u, double *v, float x, float alpha, float beta)
+{
+    sgd_step_f64(k, u, v, x, alpha, beta);
+}
+
 /* ---------------------------------------------------------------------- */
 /* One epoch: strata s = 0..p-1 in ascending order; inside a stratum the   */
 /* blocks b = 0..p-1 (any order gives the same bits because the blocks of  */
@@ -137,6 +158,16 @@ static void run_block(int32_t k, int64_t q, const int32_t *rows, const int32_t *
     for (int64_t t = block_ptr[q]; t < block_ptr[q + 1]; ++t) {
         int32_t e = perm[t];
         sgd_step(k, U + (int64_t)rows[e] * k, V + (int64_t)cols[e] * k, vals[e], alpha, beta);
+    }
+}
+
+static void run_block_f64(int32_t k, int64_t q, const int32_t *rows, const int32_t *cols,
+                          const float *vals, const int64_t *block_ptr, const int32_t *perm,
+                          double *U, double *V, float alpha, float beta)
+{
+    for (int64_t t = block_ptr[q]; t < block_ptr[q + 1]; ++t) {
+        int32_t e = perm[t];
+        sgd_step_f64(k, U + (int64_t)rows[e] * k, V + (int64_t)cols[e] * k, vals[e], alpha, beta);
     }
 }
 
@@ -173,6 +204,7 @@ struct mt_ctx {
     const int32_t *rows, *cols; const float *vals;
     const int64_t *block_ptr; const int32_t *perm;
     float *U, *V; float alpha, beta;
+    double *U64, *V64;  /* non-NULL: the binary64 schedule */
     pthread_barrier_t barrier;
     pthread_mutex_t gate_mu; pthread_cond_t gate_cv; int gate; /* 0 wait, 1 go, -1 abort */
 };
@@ -188,20 +220,39 @@ static void *mt_worker(void *arg_)
     pthread_mutex_unlock(&c->gate_mu);
     if (go < 0) return NULL;
     for (int64_t s = 0; s < c->p; ++s) {
-        for (int64_t b = a->tid; b < c->p; b += c->nthreads)
-            run_block(c->k, s * c->p + b, c->rows, c->cols, c->vals, c->block_ptr, c->perm,
-                      c->U, c->V, c->alpha, c->beta);
+        for (int64_t b = a->tid; b < c->p; b += c->nthreads) {
+            if (c->U64)
+                run_block_f64(c->k, s * c->p + b, c->rows, c->cols, c->vals, c->block_ptr,
+                              c->perm, c->U64, c->V64, c->alpha, c->beta);
+            else
+                run_block(c->k, s * c->p + b, c->rows, c->cols, c->vals, c->block_ptr, c->perm,
+                          c->U, c->V, c->alpha, c->beta);
+        }
         pthread_barrier_wait(&c->barrier);
     }
     return NULL;
 }
 
-int oracle_epoch_mt(int64_t p, int32_t k, const int32_t *rows, const int32_t *cols,
+static void epoch_seq(int64_t p, int32_t k, const int32_t *rows, const int32_t *cols,
+                      const float *vals, const int64_t *block_ptr, const int32_t *perm,
+                      float *U, float *V, double *U64, double *V64, float alpha, float beta)
+{
+    if (!U64) {
+        oracle_epoch(p, k, rows, cols, vals, block_ptr, perm, U, V, alpha, beta);
+        return;
+    }
+    for (int64_t s = 0; s < p; ++s)
+        for (int64_t b = 0; b < p; ++b)
+            run_block_f64(k, s * p + b, rows, cols, vals, block_ptr, perm, U64, V64, alpha, beta);
+}
+
+static int epoch_mt(int64_t p, int32_t k, const int32_t *rows, const int32_t *cols,
                     const float *vals, const int64_t *block_ptr, const int32_t *perm,
-                    float *U, float *V, float alpha, float beta, int32_t nthreads)
+                    float *U, float *V, double *U64, double *V64, float alpha, float beta,
+                    int32_t nthreads)
 {
     if (nthreads <= 1) {
-        oracle_epoch(p, k, rows, cols, vals, block_ptr, perm, U, V, alpha, beta);
+        epoch_seq(p, k, rows, cols, vals, block_ptr, perm, U, V, U64, V64, alpha, beta);
         return 1;
     }
     struct mt_ctx *c = (struct mt_ctx *)calloc(1, sizeof(struct mt_ctx));
@@ -209,13 +260,14 @@ int oracle_epoch_mt(int64_t p, int32_t k, const int32_t *rows, const int32_t *co
     struct mt_arg *args = (struct mt_arg *)malloc(sizeof(struct mt_arg) * (size_t)nthreads);
     if (!c || !th || !args) {
         free(c); free(th); free(args);
-        oracle_epoch(p, k, rows, cols, vals, block_ptr, perm, U, V, alpha, beta);
+        epoch_seq(p, k, rows, cols, vals, block_ptr, perm, U, V, U64, V64, alpha, beta);
         return 1;
     }
     c->p = p; c->k = k; c->nthreads = nthreads;
     c->rows = rows; c->cols = cols; c->vals = vals;
     c->block_ptr = block_ptr; c->perm = perm;
     c->U = U; c->V = V; c->alpha = alpha; c->beta = beta;
+    c->U64 = U64; c->V64 = V64;
     pthread_barrier_init(&c->barrier, NULL, (unsigned)nthreads);
     pthread_mutex_init(&c->gate_mu, NULL);
     pthread_cond_init(&c->gate_cv, NULL);
@@ -233,7 +285,7 @@ int oracle_epoch_mt(int64_t p, int32_t k, const int32_t *rows, const int32_t *co
     for (int t = 0; t < started; ++t) pthread_join(th[t], NULL);
     int used = nthreads;
     if (started != nthreads) {
-        oracle_epoch(p, k, rows, cols, vals, block_ptr, perm, U, V, alpha, beta);
+        epoch_seq(p, k, rows, cols, vals, block_ptr, perm, U, V, U64, V64, alpha, beta);
         used = 1;
     }
     pthread_barrier_destroy(&c->barrier);
@@ -241,6 +293,25 @@ int oracle_epoch_mt(int64_t p, int32_t k, const int32_t *rows, const int32_t *co
     pthread_cond_destroy(&c->gate_cv);
     free(c); free(th); free(args);
     return used; /* number of threads that did the work */
+}
+
+int oracle_epoch_mt(int64_t p, int32_t k, const int32_t *rows, const int32_t *cols,
+                    const float *vals, const int64_t *block_ptr, const int32_t *perm,
+                    float *U, float *V, float alpha, float beta, int32_t nthreads)
+{
+    return epoch_mt(p, k, rows, cols, vals, block_ptr, perm, U, V, NULL, NULL, alpha, beta,
+                    nthreads);
+}
+
+/* The epoch in binary64: same schedule and operation order, factors held in
+ * double (U64, V64), ratings and the step sizes widened exactly from their
+ * binary32 values.  nthreads <= 1 runs it on the calling thread. */
+int oracle_epoch_mt_f64(int64_t p, int32_t k, const int32_t *rows, const int32_t *cols,
+                        const float *vals, const int64_t *block_ptr, const int32_t *perm,
+                        double *U64, double *V64, float alpha, float beta, int32_t nthreads)
+{
+    return epoch_mt(p, k, rows, cols, vals, block_ptr, perm, NULL, NULL, U64, V64, alpha, beta,
+                    nthreads);
 }
 
 /* ---------------------------------------------------------------------- */

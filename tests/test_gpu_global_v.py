@@ -133,4 +133,6 @@ def test_out_of_core_global_v():
     a = gpu_run(w, 2, v_staging=GLOBAL, budget=budget)
     b = gpu_run(w, 2, v_staging=LDS)
     assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
-    assert a[2] == b[2]
+    # the streamed RMSE pass adds its fp64 partial sums in another grouping
+    for x, y in zip(a[2], b[2]):
+        assert abs(x - y) <= 1e-12 * y

@@ -118,3 +118,27 @@ def test_ooc_budget_below_two_strata():
         mdl.load_coo(w.rows, w.cols, w.vals)
         mdl.epoch(w.alpha, w.beta)
         assert np.isfinite(mdl.rmse())
+
+
+def test_ooc_workload_shape_parity():
+    """The out-of-core workload's shape (n = 10M, m = 5M, k = 64, p = 4096:
+    1221 columns per block, so V stays in global memory) at 50M ratings,
+    streamed under a budget of a third of its records: bucketing bit-exact
+    and one epoch within 1e-4 of the oracle."""
+    import os
+    import oracle
+    w = make_config("ooc", nnz=50_000_000,
+                    cache_dir=os.environ.get("BGMF_WORKLOAD_CACHE", "/tmp/bgmf_cache"))
+    print(f"ooc-shaped workload: nnz={w.nnz}", flush=True)
+    U, V, hist, bp, perm, slots, chunks, resident = _run(w, 1, budget=w.nnz * 8 // 3)
+    print(f"gpu: slots={slots} chunks={chunks} resident={resident} rmse={hist}", flush=True)
+    assert slots == 3 and resident < w.p
+    bp_ref, perm_ref = oracle.bucket(w.n, w.m, w.p, w.rows, w.cols)
+    assert np.array_equal(bp, bp_ref) and np.array_equal(perm, perm_ref)
+    U_ref, V_ref = w.U0.copy(), w.V0.copy()
+    oracle.epoch_mt(w.p, w.rows, w.cols, w.vals, bp_ref, perm_ref, U_ref, V_ref, w.alpha, w.beta,
+                    min(16, os.cpu_count() or 1))
+    r_ref = oracle.rmse(w.rows, w.cols, w.vals, U_ref, V_ref)
+    print(f"oracle rmse={r_ref}", flush=True)
+    assert row_rel_err(U, U_ref) <= TOL and row_rel_err(V, V_ref) <= TOL
+    assert abs(hist[0] - r_ref) <= TOL * r_ref

@@ -1,0 +1,95 @@
+"""The out-of-core workload at its full size: 2e9 ratings (n = 10M, m = 5M,
+k = 64, p = 4096) with the ratings streamed from pinned host memory under a
+16e9-byte device budget.
+
+Opt-in (set BGMF_OOC_FULL=1): it needs about 150 GB of host memory and ten
+minutes, mostly drawing the workload.  At this size the oracle's bucketing
+and epoch are not run (the same shape is checked against the oracle at 50M
+ratings in test_gpu_ooc.py); instead:
+  * the bucketing is checked exactly against its definition: block_ptr is
+    the running count of ratings per slot q = s p + R, perm is a
+    permutation, and perm lists the ratings in ascending (q, row, input
+    position) order, which is the unique stable order the layout promises;
+  * the streamed epoch is bit-identical to the same epoch with all ratings
+    on the device, and its RMSE is finite and below the initial one.
+"""
+import os
+import time
+
+import numpy as np
+import pytest
+
+from workloads import make_config
+from workloads.synth import OOC_BUDGET_BYTES
+
+pytestmark = [
+    pytest.mark.gpu,
+    pytest.mark.timeout(1100),
+    pytest.mark.skipif(os.environ.get("BGMF_OOC_FULL") != "1",
+                       reason="2e9-rating run: opt in with BGMF_OOC_FULL=1"),
+]
+
+T0 = time.time()
+
+
+def _log(msg):
+    print(f"[{time.time() - T0:7.1f} s] {msg}", flush=True)
+
+
+def _run(w, budget):
+    from paper_2304_13724_amd import bgmf
+    with bgmf.Model(w.n, w.m, w.k, w.p) as mdl:
+        mdl.set_option(bgmf.BGMF_OPT_RATINGS_BUDGET, budget)
+        mdl.set_factors(w.U0, w.V0)
+        t = time.time()
+        mdl.load_coo(w.rows, w.cols, w.vals)
+        info = dict(load_s=round(time.time() - t, 1),
+                    slots=mdl.get_option(bgmf.BGMF_OPT_STREAM_SLOTS),
+                    chunks=mdl.get_option(bgmf.BGMF_OPT_STREAM_CHUNKS),
+                    resident=mdl.get_option(bgmf.BGMF_OPT_RESIDENT_STRATA),
+                    placement=mdl.get_option(bgmf.BGMF_OPT_PLACEMENT))
+        r0 = mdl.rmse()
+        mdl.epoch(w.alpha, w.beta)
+        r1 = mdl.rmse()
+        info["epoch_ms"], info["rmse_ms"] = [round(x, 1) for x in mdl.timing()]
+        bp, perm = mdl.get_layout() if budget else (None, None)
+        U, V = mdl.get_factors()
+    _log(f"budget={budget}: {info} rmse {r0} -> {r1}")
+    return U, V, r0, r1, bp, perm
+
+
+def _check_layout(w, bp, perm):
+    n, m, p = w.n, w.m, w.p
+    q = np.empty(w.nnz, dtype=np.int64)
+    step = 100_000_000
+    for a in range(0, w.nnz, step):
+        r = w.rows[a:a + step].astype(np.int64) * p // n
+        c = w.cols[a:a + step].astype(np.int64) * p // m
+        q[a:a + step] = ((c - r) % p) * p + r
+    counts = np.bincount(q, minlength=p * p)
+    assert bp[0] == 0 and np.array_equal(np.diff(bp), counts)
+    _log("block_ptr = running slot counts")
+    seen = np.zeros(w.nnz, dtype=np.bool_)
+    seen[perm] = True
+    assert seen.all() and perm.min() >= 0
+    del seen
+    _log("perm is a permutation")
+    for a in range(0, w.nnz - 1, step):
+        e = perm[a:a + step + 1].astype(np.int64)
+        qq, rr = q[e], w.rows[e]
+        later = (qq[1:] > qq[:-1]) | ((qq[1:] == qq[:-1]) & (
+            (rr[1:] > rr[:-1]) | ((rr[1:] == rr[:-1]) & (e[1:] > e[:-1]))))
+        assert later.all(), a
+    _log("perm is in ascending (slot, row, input position) order")
+
+
+def test_ooc_workload_full():
+    w = make_config("ooc", log=_log)
+    _log(f"workload drawn: nnz={w.nnz}")
+    Us, Vs, r0, r1, bp, perm = _run(w, OOC_BUDGET_BYTES)
+    _check_layout(w, bp, perm)
+    del bp, perm
+    assert np.isfinite(r1) and r1 < r0
+    Ui, Vi, r0i, r1i, _, _ = _run(w, 0)
+    assert np.array_equal(Us, Ui) and np.array_equal(Vs, Vi)
+    assert abs(r1 - r1i) <= 1e-12 * r1i

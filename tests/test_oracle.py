@@ -250,6 +250,65 @@ def test_multithreaded_epoch_is_bit_identical(threads):
     assert np.array_equal(U1, U2) and np.array_equal(V1, V2)
 
 
+# ---------------------------------------------------------------- binary64 reference
+
+def test_update_f64_worked_example(golden_dir):
+    """The worked update is exact in binary32, so binary64 gives the same numbers."""
+    g = json.load(open(os.path.join(golden_dir, "update_worked_example.json")))
+    u, v = oracle.sgd_update_f64(g["u"], g["v"], g["x"], g["alpha"], g["beta"])
+    assert u.tolist() == g["u_new"]
+    assert v.tolist() == g["v_new"]
+
+
+def _plain_sgd_f64(rows, cols, vals, U, V, alpha, beta):
+    """Textbook sequential SGD in Python floats (binary64) over ratings in
+    (row, input index) order, without the block grid; alpha and beta are
+    first rounded to binary32, as every caller passes them."""
+    a, b = float(np.float32(alpha)), float(np.float32(beta))
+    order = sorted(range(len(rows)), key=lambda e: (int(rows[e]), e))
+    for e in order:
+        i, j, x = int(rows[e]), int(cols[e]), float(vals[e])
+        u = [float(t) for t in U[i]]
+        v = [float(t) for t in V[j]]
+        acc = 0.0
+        for g in range(len(u)):
+            acc = acc + u[g] * v[g]
+        err = x - acc
+        U[i, :] = [u[g] + a * ((err * v[g]) - (b * u[g])) for g in range(len(u))]
+        V[j, :] = [v[g] + a * ((err * u[g]) - (b * v[g])) for g in range(len(v))]
+
+
+def test_f64_epoch_p1_is_plain_sequential_sgd():
+    n, m, k = 30, 20, 16
+    rows, cols, vals, U, V = _small(n, m, 250, k, 1, 12)
+    U1, V1 = U.astype(np.float64), V.astype(np.float64)
+    bp, perm = oracle.bucket(n, m, 1, rows, cols)
+    oracle.epoch_f64(1, rows, cols, vals, bp, perm, U1, V1, 0.05, 0.02)
+    U2, V2 = U.astype(np.float64), V.astype(np.float64)
+    _plain_sgd_f64(rows, cols, vals, U2, V2, 0.05, 0.02)
+    assert np.array_equal(U1, U2) and np.array_equal(V1, V2)
+
+
+@pytest.mark.parametrize("threads", [2, 5])
+def test_f64_epoch_threads_and_distance_to_f32(threads):
+    """Threads leave the binary64 epoch bit-identical; the binary32 epoch
+    differs from it only by rounding (relative row error far below 1e-4 on
+    this workload, and not zero)."""
+    from helpers import row_rel_err
+    w = make_config("medium", nnz=200_000, n=5_000, m=800, p=16, k=32)
+    bp, perm = oracle.bucket(w.n, w.m, w.p, w.rows, w.cols)
+    U32, V32 = w.U0.copy(), w.V0.copy()
+    oracle.epoch(w.p, w.rows, w.cols, w.vals, bp, perm, U32, V32, w.alpha, w.beta)
+    Ua, Va = w.U0.astype(np.float64), w.V0.astype(np.float64)
+    Ub, Vb = Ua.copy(), Va.copy()
+    assert oracle.epoch_f64(w.p, w.rows, w.cols, w.vals, bp, perm, Ua, Va, w.alpha, w.beta) == 1
+    assert oracle.epoch_f64(w.p, w.rows, w.cols, w.vals, bp, perm, Ub, Vb, w.alpha, w.beta,
+                            threads) == threads
+    assert np.array_equal(Ua, Ub) and np.array_equal(Va, Vb)
+    d = max(row_rel_err(U32, Ua), row_rel_err(V32, Va))
+    assert 0 < d < 1e-5, d
+
+
 def test_planted_low_rank_rmse_decreases_to_noise_floor():
     w = make_config("tiny", keep_planted=True)
     bp, perm = oracle.bucket(w.n, w.m, w.p, w.rows, w.cols)

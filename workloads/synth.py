@@ -67,7 +67,8 @@ class Workload:
 
 # Parameters of the five benchmark workloads (sizes, degree structure, value
 # model, factor width k, grid p, step sizes, epochs, seeds) and of the
-# paper's Table 1 matrix.
+# paper's Table 1 matrix.  The "ooc" workload is meant to be run with its
+# ratings streamed from host memory under OOC_BUDGET_BYTES of device memory.
 CONFIGS = {
     "tiny": dict(n=2_000, m=1_000, nnz=100_000, structure="uniform", values="int5", rank=8,
                  noise=0.5, k=16, p=4, alpha=0.01, beta=0.05, epochs=5, seed=1),
@@ -80,9 +81,15 @@ CONFIGS = {
     "vlarge": dict(n=1_000_000, m=625_000, nnz=250_000_000, structure="powerlaw",
                    user_deg=("zipf", 1.1), item_zipf=1.1, values="cont100", rank=64, noise=5.0,
                    k=128, p=2048, alpha=0.002, beta=0.02, epochs=10, seed=4),
+    "ooc": dict(n=10_000_000, m=5_000_000, nnz=2_000_000_000, structure="powerlaw",
+                user_deg=("zipf", 1.1), item_zipf=1.1, values="int5", rank=32, noise=0.5,
+                k=64, p=4096, alpha=0.005, beta=0.05, epochs=3, seed=5),
     "table1": dict(n=1024, m=1024, nnz=1024 * 1024, structure="dense", values="uint", lo=1, hi=30,
                    k=16, p=32, alpha=2e-4, beta=5e-3, epochs=6, seed=6),
 }
+
+
+OOC_BUDGET_BYTES = 16_000_000_000
 
 
 def _zipf_weights(count: int, a: float) -> np.ndarray:
@@ -206,11 +213,13 @@ def make(name: str, n: int, m: int, nnz: int, k: int, p: int, alpha: float, beta
          epochs: int, seed: int, structure: str, values: str, rank: int = 8, noise: float = 0.5,
          user_deg=("zipf", 1.0), item_zipf: float = 1.1, lo: int = 1, hi: int = 30,
          seed_init: Optional[int] = None, seed_order: Optional[int] = None,
-         cache_dir: Optional[str] = None, keep_planted: bool = False) -> Workload:
+         cache_dir: Optional[str] = None, keep_planted: bool = False,
+         log=None) -> Workload:
     """Draw one workload.  Seeds: data ``seed``; init ``seed_init`` (default
     100 + seed); order shuffle ``seed_order`` (default 200 + seed).  With
     ``keep_planted`` the noiseless planted prediction of every rating is kept
-    (in COO order) for noise-floor estimates."""
+    (in COO order) for noise-floor estimates.  ``log``, if given, is called
+    with a short message after each generation phase."""
     seed_init = 100 + seed if seed_init is None else seed_init
     seed_order = 200 + seed if seed_order is None else seed_order
     params = dict(n=n, m=m, nnz=nnz, k=k, p=p, seed=seed, structure=structure, values=values,
@@ -221,7 +230,7 @@ def make(name: str, n: int, m: int, nnz: int, k: int, p: int, alpha: float, beta
     arrays = _load_cache(cache_dir, tag) if cache_dir else None
     if arrays is None:
         arrays = _draw(n, m, nnz, k, seed, structure, values, rank, noise, user_deg, item_zipf,
-                       lo, hi, seed_init, seed_order)
+                       lo, hi, seed_init, seed_order, log or (lambda msg: None))
         if cache_dir:
             _save_cache(cache_dir, tag, arrays)
     rows, cols, vals, U0, V0, planted = arrays
@@ -230,7 +239,7 @@ def make(name: str, n: int, m: int, nnz: int, k: int, p: int, alpha: float, beta
 
 
 def _draw(n, m, nnz, k, seed, structure, values, rank, noise, user_deg, item_zipf, lo, hi,
-          seed_init, seed_order):
+          seed_init, seed_order, log):
     rng = np.random.Generator(np.random.PCG64(seed))
     if structure == "uniform":
         if nnz > n * m:
@@ -248,6 +257,7 @@ def _draw(n, m, nnz, k, seed, structure, values, rank, noise, user_deg, item_zip
         rows = (cells // m).astype(np.int32)
         cols = (cells % m).astype(np.int32)
         del cells
+    log(f"cells drawn: {rows.shape[0]}")
 
     if values == "int5":
         z = _planted_dot(rng, rows, cols, n, m, rank)
@@ -267,10 +277,13 @@ def _draw(n, m, nnz, k, seed, structure, values, rank, noise, user_deg, item_zip
     else:
         raise ValueError(values)
     z = None
+    log("values drawn")
 
     order = np.random.Generator(np.random.PCG64(seed_order)).permutation(rows.shape[0])
+    log("order drawn")
     rows, cols, vals, planted = rows[order], cols[order], vals[order], planted[order]
     del order
+    log("ratings shuffled")
     U0, V0 = init_factors(n, m, k, seed_init)
     return (np.ascontiguousarray(rows), np.ascontiguousarray(cols), np.ascontiguousarray(vals),
             U0, V0, np.ascontiguousarray(planted))
