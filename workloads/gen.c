@@ -142,3 +142,80 @@ void gen_normal(int64_t count, uint64_t seed, double *out)
         out[e] = sqrt(-2.0 * log(u1)) * cos(6.283185307179586 * u2);
     }
 }
+
+/*
+ * Uniformly random permutation of 0..count-1 that does not depend on the
+ * number of threads.  Every index draws a bucket label from its own stream
+ * (seed, index); the indices are grouped by label (in ascending index order
+ * inside a bucket), and each bucket is then shuffled by Fisher-Yates with
+ * its own stream (seed, count + bucket).  Independent uniform labels plus a
+ * uniform order inside every bucket make every permutation equally likely
+ * (all indices are exchangeable).  The grouping runs over a fixed number of
+ * index chunks so that its result is the same for any thread count.
+ * Returns 0, or -1 on allocation failure.
+ */
+#define PERM_BUCKETS 16384
+#define PERM_CHUNKS 256
+
+static inline uint32_t perm_bucket(uint64_t seed, int64_t i)
+{
+    uint64_t st = stream_seed(seed, (uint64_t)i);
+    return (uint32_t)(splitmix64(&st) >> 50);  /* top 14 bits: 0 .. 16383 */
+}
+
+int gen_permutation(int64_t count, uint64_t seed, int64_t *perm)
+{
+    int64_t *cnt = (int64_t *)calloc((size_t)PERM_CHUNKS * PERM_BUCKETS, sizeof(int64_t));
+    int64_t *start = (int64_t *)malloc(sizeof(int64_t) * (PERM_BUCKETS + 1));
+    if (!cnt || !start) {
+        free(cnt);
+        free(start);
+        return -1;
+    }
+    const int64_t per = (count + PERM_CHUNKS - 1) / PERM_CHUNKS;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int c = 0; c < PERM_CHUNKS; ++c) {
+        int64_t *h = cnt + (int64_t)c * PERM_BUCKETS;
+        const int64_t lo = (int64_t)c * per, hi = lo + per < count ? lo + per : count;
+        for (int64_t i = lo; i < hi; ++i) h[perm_bucket(seed, i)] += 1;
+    }
+    /* exclusive offsets in (bucket, chunk) order */
+    int64_t run = 0;
+    for (int b = 0; b < PERM_BUCKETS; ++b) {
+        start[b] = run;
+        for (int c = 0; c < PERM_CHUNKS; ++c) {
+            int64_t v = cnt[(int64_t)c * PERM_BUCKETS + b];
+            cnt[(int64_t)c * PERM_BUCKETS + b] = run;
+            run += v;
+        }
+    }
+    start[PERM_BUCKETS] = run;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int c = 0; c < PERM_CHUNKS; ++c) {
+        int64_t *h = cnt + (int64_t)c * PERM_BUCKETS;
+        const int64_t lo = (int64_t)c * per, hi = lo + per < count ? lo + per : count;
+        for (int64_t i = lo; i < hi; ++i) perm[h[perm_bucket(seed, i)]++] = i;
+    }
+#pragma omp parallel for schedule(dynamic, 16)
+    for (int b = 0; b < PERM_BUCKETS; ++b) {
+        uint64_t st = stream_seed(seed, (uint64_t)count + (uint64_t)b);
+        int64_t *a = perm + start[b];
+        for (int64_t j = start[b + 1] - start[b] - 1; j > 0; --j) {
+            int64_t r = (int64_t)(uniform01(&st) * (double)(j + 1));
+            if (r > j) r = j;
+            int64_t t = a[j];
+            a[j] = a[r];
+            a[r] = t;
+        }
+    }
+    free(cnt);
+    free(start);
+    return 0;
+}
+
+/* dst[e] = src[perm[e]] for 4-byte elements (int32 or float32). */
+void gen_gather32(int64_t count, const int64_t *perm, const uint32_t *src, uint32_t *dst)
+{
+#pragma omp parallel for schedule(static)
+    for (int64_t e = 0; e < count; ++e) dst[e] = src[perm[e]];
+}

@@ -172,6 +172,23 @@ def _normal(count, seed):
     return out
 
 
+def _permutation(count, seed):
+    """Seeded uniform permutation of 0..count-1 (int64), the same for any
+    thread count (see gen_permutation in gen.c)."""
+    out = np.empty(count, dtype=np.int64)
+    if _genlib().gen_permutation(count, ctypes.c_uint64(seed * 2654435761 + 11), _ptr(out)) != 0:
+        raise MemoryError("gen_permutation failed")
+    return out
+
+
+def _gather(order, a):
+    """a[order] for a 4-byte array, in parallel."""
+    assert a.dtype.itemsize == 4
+    out = np.empty_like(a)
+    _genlib().gen_gather32(a.shape[0], _ptr(order), _ptr(np.ascontiguousarray(a)), _ptr(out))
+    return out
+
+
 _GEN = None
 _HERE = os.path.dirname(os.path.abspath(__file__))
 
@@ -200,6 +217,10 @@ def _genlib():
         lib.gen_planted_dot.restype = None
         lib.gen_normal.argtypes = [I64, ctypes.c_uint64, vp]
         lib.gen_normal.restype = None
+        lib.gen_permutation.argtypes = [I64, ctypes.c_uint64, vp]
+        lib.gen_permutation.restype = ctypes.c_int
+        lib.gen_gather32.argtypes = [I64, vp, vp, vp]
+        lib.gen_gather32.restype = None
         _GEN = lib
     return _GEN
 
@@ -224,7 +245,7 @@ def make(name: str, n: int, m: int, nnz: int, k: int, p: int, alpha: float, beta
     seed_order = 200 + seed if seed_order is None else seed_order
     params = dict(n=n, m=m, nnz=nnz, k=k, p=p, seed=seed, structure=structure, values=values,
                   rank=rank, noise=noise, user_deg=list(user_deg), item_zipf=item_zipf, lo=lo,
-                  hi=hi, seed_init=seed_init, seed_order=seed_order, version=3)
+                  hi=hi, seed_init=seed_init, seed_order=seed_order, version=4)
     tag = hashlib.sha1(json.dumps(params, sort_keys=True).encode()).hexdigest()[:16]
     cache_dir = cache_dir or os.environ.get("BGMF_WORKLOAD_CACHE")
     arrays = _load_cache(cache_dir, tag) if cache_dir else None
@@ -279,9 +300,9 @@ def _draw(n, m, nnz, k, seed, structure, values, rank, noise, user_deg, item_zip
     z = None
     log("values drawn")
 
-    order = np.random.Generator(np.random.PCG64(seed_order)).permutation(rows.shape[0])
+    order = _permutation(rows.shape[0], seed_order)
     log("order drawn")
-    rows, cols, vals, planted = rows[order], cols[order], vals[order], planted[order]
+    rows, cols, vals, planted = (_gather(order, a) for a in (rows, cols, vals, planted))
     del order
     log("ratings shuffled")
     U0, V0 = init_factors(n, m, k, seed_init)
