@@ -36,7 +36,11 @@ def parse():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--config", default="large")
     ap.add_argument("--nnz", type=int, default=None, help="override the rating count")
-    ap.add_argument("--schedule", type=int, default=0, help="0 persistent, 1 launch per stratum")
+    ap.add_argument("--schedule", type=int, default=0,
+                    help="0 automatic (persistent when V is staged in LDS), 1 one launch per "
+                         "stratum, 2 persistent")
+    ap.add_argument("--v-staging", type=int, default=0,
+                    help="0 automatic, 1 V slice in LDS, 2 V in global memory")
     ap.add_argument("--xcd-remap", type=int, default=1)
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle baseline sample (0 disables it)")
@@ -179,11 +183,18 @@ def main():
     mdl.set_stream(stream.cuda_stream)
     mdl.set_option(bgmf.BGMF_OPT_SCHEDULE, args.schedule)
     mdl.set_option(bgmf.BGMF_OPT_XCD_REMAP, args.xcd_remap)
+    mdl.set_option(bgmf.BGMF_OPT_V_STAGING, args.v_staging)
     mdl.set_factors(w.U0, w.V0)
     t0 = time.perf_counter()
     mdl.load_coo(w.rows, w.cols, w.vals)
     t_load = time.perf_counter() - t0
     chain = [int(x) for x in mdl.chain_stats()]
+    placement = mdl.get_option(bgmf.BGMF_OPT_PLACEMENT)
+    kp = 16
+    while kp < w.k:
+        kp *= 2
+    kernel = (f"k_sgd_lds<{kp}>" if placement & 1 else f"k_sgd_gv<{kp}>") + (
+        " (one launch = one epoch)" if placement & 4 else " (one launch per stratum)")
     log(f"load+bucket {t_load:.2f} s; chain: max col-block {chain[0]}, max row-block {chain[1]}, "
         f"sum of stratum maxima {chain[2]}, non-empty blocks {chain[3]}")
 
@@ -247,7 +258,7 @@ def main():
             "workload": (f"{args.config}: n={w.n} users, m={w.m} items, {nnz} ratings "
                          f"(lognormal user degree, Zipf(1.2) items), k={w.k}, p={w.p}, "
                          f"alpha={w.alpha}, beta={w.beta}; step = one epoch + RMSE pass"),
-            "schedule": "persistent" if args.schedule == 0 else "launch per stratum",
+            "sweep": kernel,
         },
         "roofline": {
             "bound": "hbm",
@@ -256,7 +267,7 @@ def main():
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBS,
             "traffic": traffic,
-            "kernel": "k_sgd_lds<64> (one launch = one epoch)",
+            "kernel": kernel,
             "bytes_per_update": b_alg,
         },
         "cpu_baseline": cpu,
