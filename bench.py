@@ -39,6 +39,9 @@ def parse():
     ap.add_argument("--schedule", type=int, default=0,
                     help="0 automatic (persistent when V is staged in LDS), 1 one launch per "
                          "stratum, 2 persistent")
+    ap.add_argument("--passes", type=int, default=1,
+                    help="GPU_STEPS: sweeps of each block per epoch (an epoch then makes "
+                         "passes x nnz updates)")
     ap.add_argument("--v-staging", type=int, default=0,
                     help="0 automatic, 1 V slice in LDS, 2 V in global memory")
     ap.add_argument("--xcd-remap", type=int, default=1)
@@ -184,6 +187,7 @@ def main():
     mdl.set_option(bgmf.BGMF_OPT_SCHEDULE, args.schedule)
     mdl.set_option(bgmf.BGMF_OPT_XCD_REMAP, args.xcd_remap)
     mdl.set_option(bgmf.BGMF_OPT_V_STAGING, args.v_staging)
+    mdl.set_option(bgmf.BGMF_OPT_BLOCK_PASSES, args.passes)
     mdl.set_factors(w.U0, w.V0)
     t0 = time.perf_counter()
     mdl.load_coo(w.rows, w.cols, w.vals)
@@ -231,10 +235,11 @@ def main():
     ms_per_step = total_ms / args.steps
 
     nnz = w.nnz
-    value = nnz * args.steps / (total_ms / 1e3)
+    upd = nnz * args.passes  # updates per epoch
+    value = upd * args.steps / (total_ms / 1e3)
     b_alg = 12 + 16 * w.k
     sweep_avg = float(np.mean(sweep_ms))
-    achieved = nnz * b_alg / (sweep_avg / 1e3) / 1e9
+    achieved = upd * b_alg / (sweep_avg / 1e3) / 1e9
     traffic = None
     if args.traffic and os.path.exists(args.traffic):
         tr = json.load(open(args.traffic))
@@ -257,7 +262,8 @@ def main():
         "config": {
             "workload": (f"{args.config}: n={w.n} users, m={w.m} items, {nnz} ratings "
                          f"(lognormal user degree, Zipf(1.2) items), k={w.k}, p={w.p}, "
-                         f"alpha={w.alpha}, beta={w.beta}; step = one epoch + RMSE pass"),
+                         f"alpha={w.alpha}, beta={w.beta}; step = one epoch + RMSE pass"
+                         + (f"; {args.passes} passes per block" if args.passes > 1 else "")),
             "sweep": kernel,
         },
         "roofline": {
@@ -272,7 +278,7 @@ def main():
         },
         "cpu_baseline": cpu,
         "sweep_ms": sweep_avg,
-        "sweep_updates_per_s": nnz / (sweep_avg / 1e3),
+        "sweep_updates_per_s": upd / (sweep_avg / 1e3),
         "rmse_pass_ms": float(np.mean(rmse_ms)),
         "load_bucket_s": t_load,
         "chain": {"max_col_block": chain[0], "max_row_block": chain[1],

@@ -22,8 +22,9 @@
  *
  * Inside a block, ratings are taken in ascending row, ties in ascending
  * input position (the order the caller passed them to bgmf_load_coo).  The
- * per-block pass count is one (Section 1.3: one pass per block is the exact
- * scheme).
+ * per-block pass count (GPU_STEPS) is one by default (Section 1.3: one pass
+ * per block is the exact scheme) and can be raised with
+ * BGMF_OPT_BLOCK_PASSES.
  *
  * Conventions for every call:
  *   - Return value: BGMF_OK (0) or a negative BGMF_E_* code; the message is
@@ -97,8 +98,9 @@ int bgmf_set_factors(bgmf_t *h, const float *U, const float *V);
 int bgmf_load_coo(bgmf_t *h, const int32_t *rows, const int32_t *cols, const float *vals,
                   int64_t nnz);
 
-/* One epoch (one CPU step of Algorithm 1 with one pass per block): strata
- * s = 0..p-1 in order, every loaded rating updated exactly once (Eq. 2-3).
+/* One epoch (one CPU step of Algorithm 1): strata s = 0..p-1 in order, every
+ * loaded rating updated once per block pass (Eq. 2-3; one pass unless
+ * BGMF_OPT_BLOCK_PASSES says otherwise).
  * alpha > 0 and beta >= 0, both finite.  Needs factors and ratings.
  * Asynchronous on the handle's stream; a device-side failure is reported by
  * the next synchronising call. */
@@ -179,6 +181,14 @@ int bgmf_factor_ptrs(bgmf_t *h, float **U_dev, float **V_dev);
                                     when the ratings stream from host memory, else 0 */
 #define BGMF_OPT_RESIDENT_STRATA 9 /* read-only: strata whose ratings stay on the
                                     device (all p unless they stream) */
+#define BGMF_OPT_BLOCK_PASSES 10 /* GPU_STEPS of Algorithm 1 (Section 1.3, Table 3):
+                                    passes of the SGD sweep over each block, its
+                                    ratings in the same order every pass, before the
+                                    block's column slice moves on; 1 (default) to
+                                    1024.  An epoch then makes passes x nnz updates.
+                                    Takes effect at the next bgmf_epoch, so a caller
+                                    can vary it from epoch to epoch (the paper's
+                                    variable block iterations). */
 int bgmf_set_option(bgmf_t *h, int32_t option, int64_t value);
 int bgmf_get_option(const bgmf_t *h, int32_t option, int64_t *value);
 

@@ -14,6 +14,7 @@ Functions follow the paper's Section 1:
   * ``sgd_update`` — one per-rating step of Eq. 2-3 (Eq. 14-15 per element)
   * ``epoch`` / ``epoch_mt`` / ``epoch_ordered`` — one CPU step of
     Algorithm 1 with one pass per block
+  * ``epoch_passes`` — the same with GPU_STEPS passes per block
   * ``rmse``     — whole-matrix RMSE used by Algorithm 1's termination test
   * ``loss``     — the objective of Eq. 1 (fp64)
   * ``sgd_update_f64`` / ``epoch_f64`` — the same step and epoch carried out
@@ -75,6 +76,12 @@ def _load():
         lib.oracle_epoch_mt_f64.argtypes = [I64, I32, i32p, i32p, f32p, i64p, i32p, f64p, f64p,
                                             F32, F32, I32]
         lib.oracle_epoch_mt_f64.restype = ctypes.c_int
+        lib.oracle_epoch_passes.argtypes = [I64, I32, i32p, i32p, f32p, i64p, i32p, f32p, f32p,
+                                            F32, F32, I32]
+        lib.oracle_epoch_passes.restype = None
+        lib.oracle_epoch_mt_passes.argtypes = [I64, I32, i32p, i32p, f32p, i64p, i32p, f32p,
+                                               f32p, F32, F32, I32, I32]
+        lib.oracle_epoch_mt_passes.restype = ctypes.c_int
         lib.oracle_rmse.argtypes = [I32, I64, i32p, i32p, f32p, f32p, f32p]
         lib.oracle_rmse.restype = F64
         lib.oracle_loss.argtypes = [I32, I64, i32p, i32p, f32p, f32p, f32p, F64]
@@ -137,6 +144,19 @@ def epoch_mt(p, rows, cols, vals, block_ptr, perm, U, V, alpha, beta, threads):
     args = _epoch_args(p, rows, cols, vals, block_ptr, perm, U, V)
     assert args[7] is U and args[8] is V
     return int(_load().oracle_epoch_mt(*args, float(alpha), float(beta), int(threads)))
+
+
+def epoch_passes(p, rows, cols, vals, block_ptr, perm, U, V, alpha, beta, passes, threads=1):
+    """One epoch with GPU_STEPS = ``passes`` (Algorithm 1, Section 1.3): every
+    block swept ``passes`` times in a row before the next; in place on U, V;
+    returns threads used."""
+    args = _epoch_args(p, rows, cols, vals, block_ptr, perm, U, V)
+    assert args[7] is U and args[8] is V
+    if threads <= 1:
+        _load().oracle_epoch_passes(*args, float(alpha), float(beta), int(passes))
+        return 1
+    return int(_load().oracle_epoch_mt_passes(*args, float(alpha), float(beta), int(passes),
+                                              int(threads)))
 
 
 def sgd_update_f64(u, v, x: float, alpha: float, beta: float):

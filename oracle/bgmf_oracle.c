@@ -180,6 +180,19 @@ void oracle_epoch(int64_t p, int32_t k, const int32_t *rows, const int32_t *cols
             run_block(k, s * p + b, rows, cols, vals, block_ptr, perm, U, V, alpha, beta);
 }
 
+/* The epoch with GPU_STEPS = passes (Algorithm 1; Section 1.3): each block
+ * is factorised passes times in a row, its ratings in the same order every
+ * time, before the next block of the row-block's sequence. */
+void oracle_epoch_passes(int64_t p, int32_t k, const int32_t *rows, const int32_t *cols,
+                         const float *vals, const int64_t *block_ptr, const int32_t *perm,
+                         float *U, float *V, float alpha, float beta, int32_t passes)
+{
+    for (int64_t s = 0; s < p; ++s)
+        for (int64_t b = 0; b < p; ++b)
+            for (int32_t g = 0; g < passes; ++g)
+                run_block(k, s * p + b, rows, cols, vals, block_ptr, perm, U, V, alpha, beta);
+}
+
 /* Same epoch with the blocks of each stratum visited in a caller-given
  * order (order[s * p + idx] = b).  Used to show that the blocks of a
  * stratum commute. */
@@ -205,6 +218,7 @@ struct mt_ctx {
     const int64_t *block_ptr; const int32_t *perm;
     float *U, *V; float alpha, beta;
     double *U64, *V64;  /* non-NULL: the binary64 schedule */
+    int32_t passes;     /* GPU_STEPS: passes over each block */
     pthread_barrier_t barrier;
     pthread_mutex_t gate_mu; pthread_cond_t gate_cv; int gate; /* 0 wait, 1 go, -1 abort */
 };
@@ -221,12 +235,14 @@ static void *mt_worker(void *arg_)
     if (go < 0) return NULL;
     for (int64_t s = 0; s < c->p; ++s) {
         for (int64_t b = a->tid; b < c->p; b += c->nthreads) {
-            if (c->U64)
-                run_block_f64(c->k, s * c->p + b, c->rows, c->cols, c->vals, c->block_ptr,
-                              c->perm, c->U64, c->V64, c->alpha, c->beta);
-            else
-                run_block(c->k, s * c->p + b, c->rows, c->cols, c->vals, c->block_ptr, c->perm,
-                          c->U, c->V, c->alpha, c->beta);
+            for (int32_t g = 0; g < c->passes; ++g) {
+                if (c->U64)
+                    run_block_f64(c->k, s * c->p + b, c->rows, c->cols, c->vals, c->block_ptr,
+                                  c->perm, c->U64, c->V64, c->alpha, c->beta);
+                else
+                    run_block(c->k, s * c->p + b, c->rows, c->cols, c->vals, c->block_ptr,
+                              c->perm, c->U, c->V, c->alpha, c->beta);
+            }
         }
         pthread_barrier_wait(&c->barrier);
     }
@@ -235,24 +251,27 @@ static void *mt_worker(void *arg_)
 
 static void epoch_seq(int64_t p, int32_t k, const int32_t *rows, const int32_t *cols,
                       const float *vals, const int64_t *block_ptr, const int32_t *perm,
-                      float *U, float *V, double *U64, double *V64, float alpha, float beta)
+                      float *U, float *V, double *U64, double *V64, float alpha, float beta,
+                      int32_t passes)
 {
     if (!U64) {
-        oracle_epoch(p, k, rows, cols, vals, block_ptr, perm, U, V, alpha, beta);
+        oracle_epoch_passes(p, k, rows, cols, vals, block_ptr, perm, U, V, alpha, beta, passes);
         return;
     }
     for (int64_t s = 0; s < p; ++s)
         for (int64_t b = 0; b < p; ++b)
-            run_block_f64(k, s * p + b, rows, cols, vals, block_ptr, perm, U64, V64, alpha, beta);
+            for (int32_t g = 0; g < passes; ++g)
+                run_block_f64(k, s * p + b, rows, cols, vals, block_ptr, perm, U64, V64, alpha,
+                              beta);
 }
 
 static int epoch_mt(int64_t p, int32_t k, const int32_t *rows, const int32_t *cols,
                     const float *vals, const int64_t *block_ptr, const int32_t *perm,
                     float *U, float *V, double *U64, double *V64, float alpha, float beta,
-                    int32_t nthreads)
+                    int32_t passes, int32_t nthreads)
 {
     if (nthreads <= 1) {
-        epoch_seq(p, k, rows, cols, vals, block_ptr, perm, U, V, U64, V64, alpha, beta);
+        epoch_seq(p, k, rows, cols, vals, block_ptr, perm, U, V, U64, V64, alpha, beta, passes);
         return 1;
     }
     struct mt_ctx *c = (struct mt_ctx *)calloc(1, sizeof(struct mt_ctx));
@@ -260,14 +279,14 @@ static int epoch_mt(int64_t p, int32_t k, const int32_t *rows, const int32_t *co
     struct mt_arg *args = (struct mt_arg *)malloc(sizeof(struct mt_arg) * (size_t)nthreads);
     if (!c || !th || !args) {
         free(c); free(th); free(args);
-        epoch_seq(p, k, rows, cols, vals, block_ptr, perm, U, V, U64, V64, alpha, beta);
+        epoch_seq(p, k, rows, cols, vals, block_ptr, perm, U, V, U64, V64, alpha, beta, passes);
         return 1;
     }
     c->p = p; c->k = k; c->nthreads = nthreads;
     c->rows = rows; c->cols = cols; c->vals = vals;
     c->block_ptr = block_ptr; c->perm = perm;
     c->U = U; c->V = V; c->alpha = alpha; c->beta = beta;
-    c->U64 = U64; c->V64 = V64;
+    c->U64 = U64; c->V64 = V64; c->passes = passes;
     pthread_barrier_init(&c->barrier, NULL, (unsigned)nthreads);
     pthread_mutex_init(&c->gate_mu, NULL);
     pthread_cond_init(&c->gate_cv, NULL);
@@ -285,7 +304,7 @@ static int epoch_mt(int64_t p, int32_t k, const int32_t *rows, const int32_t *co
     for (int t = 0; t < started; ++t) pthread_join(th[t], NULL);
     int used = nthreads;
     if (started != nthreads) {
-        epoch_seq(p, k, rows, cols, vals, block_ptr, perm, U, V, U64, V64, alpha, beta);
+        epoch_seq(p, k, rows, cols, vals, block_ptr, perm, U, V, U64, V64, alpha, beta, passes);
         used = 1;
     }
     pthread_barrier_destroy(&c->barrier);
@@ -299,8 +318,18 @@ int oracle_epoch_mt(int64_t p, int32_t k, const int32_t *rows, const int32_t *co
                     const float *vals, const int64_t *block_ptr, const int32_t *perm,
                     float *U, float *V, float alpha, float beta, int32_t nthreads)
 {
-    return epoch_mt(p, k, rows, cols, vals, block_ptr, perm, U, V, NULL, NULL, alpha, beta,
+    return epoch_mt(p, k, rows, cols, vals, block_ptr, perm, U, V, NULL, NULL, alpha, beta, 1,
                     nthreads);
+}
+
+/* Multithreaded epoch with GPU_STEPS = passes (see oracle_epoch_passes). */
+int oracle_epoch_mt_passes(int64_t p, int32_t k, const int32_t *rows, const int32_t *cols,
+                           const float *vals, const int64_t *block_ptr, const int32_t *perm,
+                           float *U, float *V, float alpha, float beta, int32_t passes,
+                           int32_t nthreads)
+{
+    return epoch_mt(p, k, rows, cols, vals, block_ptr, perm, U, V, NULL, NULL, alpha, beta,
+                    passes, nthreads);
 }
 
 /* The epoch in binary64: same schedule and operation order, factors held in
@@ -310,7 +339,7 @@ int oracle_epoch_mt_f64(int64_t p, int32_t k, const int32_t *rows, const int32_t
                         const float *vals, const int64_t *block_ptr, const int32_t *perm,
                         double *U64, double *V64, float alpha, float beta, int32_t nthreads)
 {
-    return epoch_mt(p, k, rows, cols, vals, block_ptr, perm, NULL, NULL, U64, V64, alpha, beta,
+    return epoch_mt(p, k, rows, cols, vals, block_ptr, perm, NULL, NULL, U64, V64, alpha, beta, 1,
                     nthreads);
 }
 

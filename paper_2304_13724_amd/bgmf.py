@@ -35,6 +35,7 @@ BGMF_OPT_V_STAGING = 6
 BGMF_OPT_PLACEMENT = 7
 BGMF_OPT_STREAM_CHUNKS = 8
 BGMF_OPT_RESIDENT_STRATA = 9
+BGMF_OPT_BLOCK_PASSES = 10
 
 EXPORTED = (
     "bgmf_create", "bgmf_destroy", "bgmf_last_error", "bgmf_set_stream", "bgmf_set_factors",

@@ -55,6 +55,7 @@ struct SgdParams {
   int64_t wait_ticks;        // wait limit in s_memrealtime ticks (100 MHz)
   float alpha, beta;
   int32_t xcd_remap;
+  int32_t passes;            // sweeps of each block before the next (GPU_STEPS >= 1)
 };
 constexpr int kFlagStride = 16;  // int64 words per flag (one 128-byte line)
 constexpr int kWavesPerGroup = 4;

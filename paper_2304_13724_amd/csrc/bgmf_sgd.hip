@@ -289,7 +289,7 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
     float ring[D][NV];
     uint32_t ringrow[D];
     uint2 Wn1 = make_uint2(0u, 0u);  // raw records of the next chunk
-    if (len > 0) {
+    auto prime = [&]() {
       decode(rp[lane], 0);
       Wn1 = rp[CH + lane];
 #pragma unroll
@@ -297,7 +297,8 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
         ringrow[j] = rl(wrow, j);
         ld_row<NV, 0>(ring[j], Ures, doff, ringrow[j]);
       }
-    }
+    };
+    if (len > 0) prime();
     if (s > P.s_begin) {
       // column-block C was last updated by row-block b+1 in stratum g-1
       const int nb = (b + 1 == P.p) ? 0 : b + 1;
@@ -320,6 +321,12 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
         for (int i = 0; i < 16; ++i)
           lds_st<NV>(tmp[i], ldsb, vbase + (uint32_t)min(cb + i, P.cols_max) * colbytes);
       }
+      // GPU_STEPS passes over the block, its ratings in the same order each
+      // time (Section 1.3); a later pass re-reads the U rows this wave
+      // stored in the previous one (the hardware keeps a wave's accesses to
+      // one address in order)
+      for (int pass = 0; pass < P.passes; ++pass) {
+      if (pass > 0) prime();
       uint32_t waddr = vbase + rl(wcol, 0);  // LDS address of the current column
       float vnext[NV];
       lds_ld<NV>(vnext, ldsb, waddr);
@@ -393,6 +400,7 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
       const int32_t full = len & ~(CH - 1);
       for (int32_t c = 0; c < full; c += CH) chunk(std::false_type{}, c);
       if (full < len) chunk(std::true_type{}, full);
+      }
       // publish the column slice, 16 columns per round (stores past the
       // slice are dropped)
       for (int cb = 0; cb < ncols; cb += 16) {
@@ -493,7 +501,7 @@ __global__ void __launch_bounds__(256) k_sgd_gv(SgdParams P) {
     float ring[D][NV], vring[D][NV];
     uint32_t ringrow[D];
     uint2 Wn1 = make_uint2(0u, 0u);
-    if (len > 0) {
+    auto prime = [&]() {
       decode(rp[lane >= CH ? lane - CH : 0], 0);
       Wn1 = rp[lane];  // window of chunk CH
 #pragma unroll
@@ -501,7 +509,8 @@ __global__ void __launch_bounds__(256) k_sgd_gv(SgdParams P) {
         ringrow[j] = rl(wrow, CH + j);
         ld_row<NV, 0>(ring[j], Ures, doff, ringrow[j]);
       }
-    }
+    };
+    if (len > 0) prime();
     if (s > P.s_begin) {
       const int nb = (b + 1 == P.p) ? 0 : b + 1;
       if (!wait_progress(P.flags + (int64_t)nb * kFlagStride, g, P.wait_ticks)) {
@@ -512,6 +521,11 @@ __global__ void __launch_bounds__(256) k_sgd_gv(SgdParams P) {
     if (len > 0) {
       const __amdgpu_buffer_rsrc_t Vres = __builtin_amdgcn_make_buffer_rsrc(
           P.V + c0 * k, (short)0, (int)((uint32_t)ncols * rowbytes), kBufWord3);
+      // GPU_STEPS passes over the block (Section 1.3); each pass re-reads the
+      // U and V rows this wave stored in the previous one (the hardware keeps
+      // a wave's accesses to one address in order)
+      for (int pass = 0; pass < P.passes; ++pass) {
+      if (pass > 0) prime();
 #pragma unroll
       for (int j = 0; j < D; ++j) ld_row<NV, VPOL>(vring[j], Vres, doff, rl(wcol, CH + j));
       uint32_t prev_row = 0xFFFFFFFFu;
@@ -586,6 +600,7 @@ __global__ void __launch_bounds__(256) k_sgd_gv(SgdParams P) {
       const int32_t full = len & ~(CH - 1);
       for (int32_t c = 0; c < full; c += CH) chunk(std::false_type{}, c);
       if (full < len) chunk(std::true_type{}, full);
+      }
     }
     if (P.s_end - P.s_begin > 1) publish_progress(P.flags + (int64_t)b * kFlagStride, g + 1);
   }

@@ -1,0 +1,109 @@
+"""GPU_STEPS > 1 (Algorithm 1, Section 1.3, Table 3): each block is swept
+several times in a row before its column slice moves on.  The HIP path
+against the oracle's epoch with the same pass count, for both V placements
+and schedules, streamed and in-core, and with the pass count varied from
+epoch to epoch (the paper's variable block iterations)."""
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from helpers import row_rel_err
+from workloads import make, make_config
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-4
+THREADS = min(16, os.cpu_count() or 1)
+
+CASES = {
+    "tiny": lambda: make_config("tiny"),
+    "medium_shape": lambda: make_config("medium", n=7_000, m=1_000, nnz=300_000, p=32),
+    "large_shape": lambda: make_config("large", n=48_000, m=1_800, nnz=1_000_000, p=128),
+    "k128_ragged": lambda: make("r", n=1_003, m=997, nnz=40_000, k=128, p=13, alpha=0.005,
+                                beta=0.05, epochs=1, seed=41, structure="uniform",
+                                values="int5", rank=4),
+}
+
+
+def _gpu(w, schedule_of_passes, v_staging=0, schedule=0, budget=0):
+    from paper_2304_13724_amd import bgmf
+    with bgmf.Model(w.n, w.m, w.k, w.p) as mdl:
+        mdl.set_option(bgmf.BGMF_OPT_V_STAGING, v_staging)
+        mdl.set_option(bgmf.BGMF_OPT_SCHEDULE, schedule)
+        mdl.set_option(bgmf.BGMF_OPT_RATINGS_BUDGET, budget)
+        mdl.set_factors(w.U0, w.V0)
+        mdl.load_coo(w.rows, w.cols, w.vals)
+        hist = []
+        for g in schedule_of_passes:
+            mdl.set_option(bgmf.BGMF_OPT_BLOCK_PASSES, g)
+            mdl.epoch(w.alpha, w.beta)
+            hist.append(mdl.rmse())
+        U, V = mdl.get_factors()
+    return U, V, hist
+
+
+def _oracle(w, schedule_of_passes):
+    bp, perm = oracle.bucket(w.n, w.m, w.p, w.rows, w.cols)
+    U, V = w.U0.copy(), w.V0.copy()
+    hist = []
+    for g in schedule_of_passes:
+        oracle.epoch_passes(w.p, w.rows, w.cols, w.vals, bp, perm, U, V, w.alpha, w.beta, g,
+                            THREADS)
+        hist.append(oracle.rmse(w.rows, w.cols, w.vals, U, V))
+    return U, V, hist
+
+
+def _close(g, o, tol=TOL):
+    assert row_rel_err(g[0], o[0]) <= tol and row_rel_err(g[1], o[1]) <= tol
+    for a, b in zip(g[2], o[2]):
+        assert abs(a - b) <= TOL * b
+
+
+@pytest.mark.parametrize("case", sorted(CASES))
+@pytest.mark.parametrize("passes", [2, 3])
+def test_passes_match_oracle(case, passes):
+    w = CASES[case]()
+    o = _oracle(w, [passes])
+    _close(_gpu(w, [passes]), o)
+
+
+@pytest.mark.parametrize("case", ["medium_shape", "k128_ragged"])
+@pytest.mark.parametrize("v_staging,schedule", [(1, 1), (2, 0), (2, 2)])
+def test_passes_placements_bit_identical(case, v_staging, schedule):
+    w = CASES[case]()
+    a = _gpu(w, [3])
+    b = _gpu(w, [3], v_staging=v_staging, schedule=schedule)
+    assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
+
+
+def test_passes_streamed_bit_identical():
+    w = CASES["large_shape"]()
+    bp, _ = oracle.bucket(w.n, w.m, w.p, w.rows, w.cols)
+    budget = 5 * (int(np.diff(bp[:: w.p]).max()) + 256) * 8
+    a = _gpu(w, [2, 3])
+    b = _gpu(w, [2, 3], budget=budget)
+    assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
+
+
+def test_variable_block_iterations():
+    """Pass counts 8, 4, 2, 1 over four epochs (a decreasing schedule of the
+    kind Table 3 compares)."""
+    w = CASES["medium_shape"]()
+    sched = [8, 4, 2, 1]
+    o = _oracle(w, sched)
+    _close(_gpu(w, sched), o, tol=3 * TOL)
+
+
+def test_pass_option_range():
+    from paper_2304_13724_amd import bgmf
+    w = CASES["tiny"]()
+    with bgmf.Model(w.n, w.m, w.k, w.p) as mdl:
+        assert mdl.get_option(bgmf.BGMF_OPT_BLOCK_PASSES) == 1
+        for bad in (0, -1, 1025):
+            with pytest.raises(bgmf.BgmfError) as ei:
+                mdl.set_option(bgmf.BGMF_OPT_BLOCK_PASSES, bad)
+            assert ei.value.code == bgmf.BGMF_E_ARG
+        mdl.set_option(bgmf.BGMF_OPT_BLOCK_PASSES, 1024)
+        assert mdl.get_option(bgmf.BGMF_OPT_BLOCK_PASSES) == 1024

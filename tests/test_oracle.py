@@ -250,6 +250,67 @@ def test_multithreaded_epoch_is_bit_identical(threads):
     assert np.array_equal(U1, U2) and np.array_equal(V1, V2)
 
 
+# ---------------------------------------------------------------- GPU_STEPS > 1
+
+def test_passes_one_is_the_epoch():
+    w = make_config("medium", nnz=100_000, n=3_000, m=600, p=8, k=16)
+    bp, perm = oracle.bucket(w.n, w.m, w.p, w.rows, w.cols)
+    U1, V1 = w.U0.copy(), w.V0.copy()
+    U2, V2 = w.U0.copy(), w.V0.copy()
+    oracle.epoch(w.p, w.rows, w.cols, w.vals, bp, perm, U1, V1, w.alpha, w.beta)
+    oracle.epoch_passes(w.p, w.rows, w.cols, w.vals, bp, perm, U2, V2, w.alpha, w.beta, 1)
+    assert np.array_equal(U1, U2) and np.array_equal(V1, V2)
+
+
+@pytest.mark.parametrize("passes", [2, 3])
+def test_passes_with_one_block_are_repeated_sweeps(passes):
+    """p = 1: the single block swept G times is G sequential SGD sweeps."""
+    n, m, k = 30, 20, 16
+    rows, cols, vals, U, V = _small(n, m, 250, k, 1, 13)
+    bp, perm = oracle.bucket(n, m, 1, rows, cols)
+    U1, V1 = U.copy(), V.copy()
+    oracle.epoch_passes(1, rows, cols, vals, bp, perm, U1, V1, 0.05, 0.02, passes)
+    U2, V2 = U.copy(), V.copy()
+    for _ in range(passes):
+        _plain_sgd_sorted_by_row(rows, cols, vals, U2, V2, 0.05, 0.02)
+    assert np.array_equal(U1, U2) and np.array_equal(V1, V2)
+
+
+def test_passes_on_single_rating_blocks():
+    """A permutation matrix with p = n = m: every block holds at most one
+    rating and every rating has its own row and column, so G passes apply
+    the update of Eq. 2-3 G times to each (u_i, v_j) independently."""
+    n = k = 16
+    rng = np.random.default_rng(14)
+    cols = rng.permutation(n).astype(np.int32)
+    rows = np.arange(n, dtype=np.int32)
+    vals = rng.integers(1, 6, n).astype(np.float32)
+    U = rng.uniform(0, 0.5, (n, k)).astype(np.float32)
+    V = rng.uniform(0, 0.5, (n, k)).astype(np.float32)
+    bp, perm = oracle.bucket(n, n, n, rows, cols)
+    U1, V1 = U.copy(), V.copy()
+    oracle.epoch_passes(n, rows, cols, vals, bp, perm, U1, V1, 0.1, 0.05, 3)
+    for i in range(n):
+        u, v = list(U[i]), list(V[cols[i]])
+        for _ in range(3):
+            u, v = pyoracle.sgd_update(u, v, vals[i], 0.1, 0.05)
+        assert U1[i].tolist() == list(np.float32(u))
+        assert V1[cols[i]].tolist() == list(np.float32(v))
+
+
+@pytest.mark.parametrize("threads", [2, 5])
+def test_passes_multithreaded_bit_identical(threads):
+    w = make_config("medium", nnz=100_000, n=3_000, m=600, p=8, k=16)
+    bp, perm = oracle.bucket(w.n, w.m, w.p, w.rows, w.cols)
+    U1, V1 = w.U0.copy(), w.V0.copy()
+    U2, V2 = w.U0.copy(), w.V0.copy()
+    oracle.epoch_passes(w.p, w.rows, w.cols, w.vals, bp, perm, U1, V1, w.alpha, w.beta, 3)
+    used = oracle.epoch_passes(w.p, w.rows, w.cols, w.vals, bp, perm, U2, V2, w.alpha, w.beta,
+                               3, threads)
+    assert used == threads
+    assert np.array_equal(U1, U2) and np.array_equal(V1, V2)
+
+
 # ---------------------------------------------------------------- binary64 reference
 
 def test_update_f64_worked_example(golden_dir):
