@@ -112,6 +112,28 @@ int bgmf_epoch(bgmf_t *h, float alpha, float beta);
  * stream. */
 int bgmf_rmse(bgmf_t *h, double *out);
 
+/* RMSE of the current factors over nnz caller-given ratings in host COO
+ * arrays (for example a held-out split, the paper's Table 2 "test RMSE"):
+ * sqrt((1/nnz) sum_e (vals[e] - u_rows[e].v_cols[e])^2), dots in fp32, sum
+ * in fp64.  The ratings need not be loaded and are not kept.  Index and
+ * value checks as in bgmf_load_coo.  Needs factors.  Allocates temporary
+ * device memory for the ratings.  Waits for the stream. */
+int bgmf_rmse_coo(bgmf_t *h, const int32_t *rows, const int32_t *cols, const float *vals,
+                  int64_t nnz, double *out);
+
+/* Algorithm 1's outer loop (CPU_STEPS = max_epochs, termination deviation
+ * delta): RMSE of the initial factors, then up to max_epochs times one epoch
+ * and its RMSE pass, stopping after the first epoch whose RMSE differs from
+ * the previous one by less than delta (Section 1.3).
+ *   *epochs_run receives the number of epochs run;
+ *   rmse_history, if not NULL, must hold max_epochs + 1 doubles and receives
+ *     the initial RMSE and the RMSE after each epoch run.
+ * max_epochs >= 1, delta >= 0 and finite; alpha, beta as for bgmf_epoch.
+ * BGMF_E_NONFINITE if an RMSE is not finite (the step diverges; the history
+ * up to that epoch is written).  Waits for the stream after every epoch. */
+int bgmf_fit(bgmf_t *h, float alpha, float beta, int32_t max_epochs, double delta,
+             int32_t *epochs_run, double *rmse_history);
+
 /* Copy the current factors to host memory (row-major n x k and m x k).
  * Either pointer may be NULL to skip it.  Waits for the stream. */
 int bgmf_get_factors(bgmf_t *h, float *U, float *V);

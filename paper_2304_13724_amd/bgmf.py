@@ -41,7 +41,7 @@ EXPORTED = (
     "bgmf_create", "bgmf_destroy", "bgmf_last_error", "bgmf_set_stream", "bgmf_set_factors",
     "bgmf_load_coo", "bgmf_epoch", "bgmf_rmse", "bgmf_get_factors", "bgmf_get_layout",
     "bgmf_sync", "bgmf_factor_ptrs", "bgmf_set_option", "bgmf_get_option", "bgmf_get_timing",
-    "bgmf_chain_stats",
+    "bgmf_chain_stats", "bgmf_rmse_coo", "bgmf_fit",
 )
 
 
@@ -76,6 +76,8 @@ def _load() -> ctypes.CDLL:
         "bgmf_get_timing": ([vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)],
                             c_int),
         "bgmf_chain_stats": ([vp, vp], c_int),
+        "bgmf_rmse_coo": ([vp, vp, vp, vp, I64, ctypes.POINTER(ctypes.c_double)], c_int),
+        "bgmf_fit": ([vp, F32, F32, I32, ctypes.c_double, ctypes.POINTER(I32), vp], c_int),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -194,6 +196,32 @@ def bgmf_chain_stats(h):
     return out
 
 
+def bgmf_rmse_coo(h, rows, cols, vals) -> float:
+    rows = np.ascontiguousarray(rows, dtype=np.int32)
+    cols = np.ascontiguousarray(cols, dtype=np.int32)
+    vals = np.ascontiguousarray(vals, dtype=np.float32)
+    if not (rows.shape == cols.shape == vals.shape and rows.ndim == 1):
+        raise ValueError("rows, cols and vals must be 1-D arrays of one length")
+    out = ctypes.c_double(math.nan)
+    _check(h, _lib.bgmf_rmse_coo(h, _ptr(rows), _ptr(cols), _ptr(vals), rows.shape[0],
+                                 ctypes.byref(out)))
+    return out.value
+
+
+def bgmf_fit(h, alpha: float, beta: float, max_epochs: int, delta: float):
+    """Returns (epochs_run, rmse_history[: epochs_run + 1])."""
+    hist = np.full(int(max_epochs) + 1, np.nan, dtype=np.float64)
+    ran = ctypes.c_int32(0)
+    rc = _lib.bgmf_fit(h, float(alpha), float(beta), int(max_epochs), float(delta),
+                       ctypes.byref(ran), _ptr(hist))
+    if rc != BGMF_OK:
+        msg = _lib.bgmf_last_error(h)
+        err = BgmfError(rc, msg.decode() if msg else "")
+        err.epochs_run, err.rmse_history = ran.value, hist[: ran.value + 1]
+        raise err
+    return ran.value, hist[: ran.value + 1]
+
+
 # --- convenience wrapper -----------------------------------------------------
 
 class Model:
@@ -257,3 +285,9 @@ class Model:
 
     def chain_stats(self):
         return bgmf_chain_stats(self.h)
+
+    def rmse_coo(self, rows, cols, vals) -> float:
+        return bgmf_rmse_coo(self.h, rows, cols, vals)
+
+    def fit(self, alpha: float, beta: float, max_epochs: int, delta: float):
+        return bgmf_fit(self.h, alpha, beta, max_epochs, delta)

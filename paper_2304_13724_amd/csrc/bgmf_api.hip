@@ -678,6 +678,87 @@ int bgmf_rmse(bgmf_t *h, double *out) {
   return BGMF_OK;
 }
 
+int bgmf_rmse_coo(bgmf_t *h, const int32_t *rows, const int32_t *cols, const float *vals,
+                  int64_t nnz, double *out) {
+  if (!h) return BGMF_E_ARG;
+  if (!rows || !cols || !vals || !out) return fail(h, BGMF_E_ARG, "bgmf_rmse_coo: null pointer");
+  if (nnz < 1 || nnz >= (1ll << 31))
+    return fail(h, BGMF_E_ARG, "nnz must be in [1, 2^31): %lld", (long long)nnz);
+  if (!h->factors_set) return fail(h, BGMF_E_STATE, "bgmf_rmse_coo: factors not set");
+  for (int64_t e = 0; e < nnz; ++e) {
+    if (rows[e] < 0 || rows[e] >= h->n || cols[e] < 0 || cols[e] >= h->m)
+      return fail(h, BGMF_E_RANGE, "rating %lld at (%d, %d) is outside the %lld x %lld matrix",
+                  (long long)e, rows[e], cols[e], (long long)h->n, (long long)h->m);
+    if (!std::isfinite(vals[e]))
+      return fail(h, BGMF_E_NONFINITE, "rating %lld has a non-finite value", (long long)e);
+  }
+  int32_t *d_rows = nullptr, *d_cols = nullptr;
+  float *d_vals = nullptr;
+  double *d_part = nullptr;
+  auto cleanup = [&]() {
+    hipFree(d_rows);
+    hipFree(d_cols);
+    hipFree(d_vals);
+    hipFree(d_part);
+  };
+  double r = 0.0;
+  hipError_t e = hipSuccess;
+  const size_t np = rmse_coo_partials_count();
+  if ((e = hipMalloc(&d_rows, (size_t)nnz * sizeof(int32_t))) == hipSuccess &&
+      (e = hipMalloc(&d_cols, (size_t)nnz * sizeof(int32_t))) == hipSuccess &&
+      (e = hipMalloc(&d_vals, (size_t)nnz * sizeof(float))) == hipSuccess &&
+      (e = hipMalloc(&d_part, (np + 1) * sizeof(double))) == hipSuccess &&
+      (e = hipMemcpyAsync(d_rows, rows, (size_t)nnz * sizeof(int32_t), hipMemcpyHostToDevice,
+                          h->stream)) == hipSuccess &&
+      (e = hipMemcpyAsync(d_cols, cols, (size_t)nnz * sizeof(int32_t), hipMemcpyHostToDevice,
+                          h->stream)) == hipSuccess &&
+      (e = hipMemcpyAsync(d_vals, vals, (size_t)nnz * sizeof(float), hipMemcpyHostToDevice,
+                          h->stream)) == hipSuccess &&
+      (e = launch_rmse_coo(d_rows, d_cols, d_vals, nnz, h->U, h->V, h->k, d_part, d_part + np,
+                           h->stream)) == hipSuccess &&
+      (e = hipMemcpyAsync(&r, d_part + np, sizeof r, hipMemcpyDeviceToHost, h->stream)) ==
+          hipSuccess)
+    e = hipStreamSynchronize(h->stream);
+  cleanup();
+  if (e != hipSuccess)
+    return fail(h, e == hipErrorOutOfMemory ? BGMF_E_NOMEM : BGMF_E_HIP, "bgmf_rmse_coo: %s",
+                hipGetErrorString(e));
+  int rc = check_device_error(h);
+  if (rc != BGMF_OK) return rc;
+  *out = r;
+  return BGMF_OK;
+}
+
+int bgmf_fit(bgmf_t *h, float alpha, float beta, int32_t max_epochs, double delta,
+             int32_t *epochs_run, double *rmse_history) {
+  if (!h) return BGMF_E_ARG;
+  if (!epochs_run) return fail(h, BGMF_E_ARG, "bgmf_fit: null epochs_run");
+  if (max_epochs < 1) return fail(h, BGMF_E_ARG, "max_epochs must be >= 1");
+  if (!std::isfinite(delta) || delta < 0.0) return fail(h, BGMF_E_ARG, "delta must be finite and >= 0");
+  *epochs_run = 0;
+  double prev = 0.0;
+  int rc = bgmf_rmse(h, &prev);
+  if (rc != BGMF_OK) return rc;
+  if (rmse_history) rmse_history[0] = prev;
+  for (int32_t e = 1; e <= max_epochs; ++e) {
+    rc = bgmf_epoch(h, alpha, beta);
+    if (rc != BGMF_OK) return rc;
+    double r = 0.0;
+    rc = bgmf_rmse(h, &r);
+    if (rc != BGMF_OK) return rc;
+    *epochs_run = e;
+    if (rmse_history) rmse_history[e] = r;
+    if (!std::isfinite(r))
+      return fail(h, BGMF_E_NONFINITE,
+                  "the RMSE is not finite after epoch %d: the step alpha = %g diverges on these "
+                  "ratings",
+                  e, (double)alpha);
+    if (std::fabs(prev - r) < delta) break;
+    prev = r;
+  }
+  return BGMF_OK;
+}
+
 int bgmf_get_factors(bgmf_t *h, float *U, float *V) {
   if (!h) return BGMF_E_ARG;
   if (U)

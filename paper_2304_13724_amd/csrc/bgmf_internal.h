@@ -94,6 +94,13 @@ hipError_t rmse_stratum_add(const uint2 *rec, int64_t rec_origin, const int64_t 
 hipError_t rmse_stratum_end(const double *partials, int32_t p, int64_t nnz, double *out,
                             hipStream_t stream);
 size_t rmse_partials_count(int32_t p);
+// RMSE over caller-given COO ratings already on the device (rows, cols,
+// vals of nnz ratings); partials must hold rmse_coo_partials_count() doubles.
+constexpr int kRmseCooGroups = 1024;
+size_t rmse_coo_partials_count();
+hipError_t launch_rmse_coo(const int32_t *rows, const int32_t *cols, const float *vals,
+                           int64_t nnz, const float *U, const float *V, int32_t k,
+                           double *partials, double *out, hipStream_t stream);
 
 // Bucketing: from device COO to the block layout.  Scratch buffers are
 // allocated by the caller (see bucket_scratch_bytes).

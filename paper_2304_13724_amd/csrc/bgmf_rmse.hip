@@ -187,6 +187,52 @@ k_rmse_stratum(const uint2 *__restrict__ rec, int64_t rec_origin,
   if (lane == 0) partials[(int64_t)blockIdx.y * p + b] += acc;
 }
 
+// RMSE over caller-given COO ratings (for example a held-out split): the
+// same dot products and fp64 squares, with a lane group per rating taken
+// from a fixed grid-stride order, and one partial per wave.
+template <int KP>
+__global__ void __launch_bounds__(256)
+k_rmse_coo(const int32_t *__restrict__ rows, const int32_t *__restrict__ cols,
+           const float *__restrict__ vals, int64_t nnz, const float *__restrict__ U,
+           const float *__restrict__ V, int32_t k, double *__restrict__ partials) {
+  constexpr int L = KP >= 64 ? 16 : KP / 4;
+  constexpr int RPS = 64 / L;
+  constexpr int Q = KP / 4;
+  constexpr int QL = (Q + L - 1) / L;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int gl = lane % L, grp = lane / L;
+  const int64_t gw = (int64_t)blockIdx.x * kWavesPerGroup + wave;
+  const int64_t stride = (int64_t)gridDim.x * kWavesPerGroup * RPS;
+  const int kq = k / 4;
+  double acc = 0.0;
+  for (int64_t t = gw * RPS + grp; t - grp < nnz; t += stride) {
+    const bool ok = t < nnz;
+    const int64_t e = ok ? t : 0;
+    const float4 *up = reinterpret_cast<const float4 *>(U + (int64_t)rows[e] * k);
+    const float4 *vp = reinterpret_cast<const float4 *>(V + (int64_t)cols[e] * k);
+    float part = 0.0f;
+#pragma unroll
+    for (int i = 0; i < QL; ++i) {
+      const int q = gl + i * L;
+      if (q < kq) {
+        const float4 a = up[q], c = vp[q];
+        part = fmaf(a.x, c.x, part);
+        part = fmaf(a.y, c.y, part);
+        part = fmaf(a.z, c.z, part);
+        part = fmaf(a.w, c.w, part);
+      }
+    }
+    part += dpp_mov<0xB1>(part);
+    if constexpr (L > 2) part += dpp_mov<0x4E>(part);
+    if constexpr (L > 4) part += dpp_mov<0x141>(part);
+    if constexpr (L > 8) part += dpp_mov<0x140>(part);
+    const float d = (ok && gl == 0) ? vals[e] - part : 0.0f;
+    acc = fma((double)d, (double)d, acc);
+  }
+  for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
+  if (lane == 0) partials[gw] = acc;
+}
+
 __global__ void k_zero(double *x, int64_t count) {
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count;
        i += (int64_t)gridDim.x * blockDim.x)
@@ -376,6 +422,31 @@ hipError_t rmse_stratum_end(const double *partials, int32_t p, int64_t nnz, doub
                             hipStream_t stream) {
   hipLaunchKernelGGL(k_rmse_final, dim3(1), dim3(256), 0, stream, partials,
                      (int64_t)kRmseStrataGroups * p, nnz, out);
+  return hipGetLastError();
+}
+
+size_t rmse_coo_partials_count() { return (size_t)kRmseCooGroups * kWavesPerGroup; }
+
+hipError_t launch_rmse_coo(const int32_t *rows, const int32_t *cols, const float *vals,
+                           int64_t nnz, const float *U, const float *V, int32_t k,
+                           double *partials, double *out, hipStream_t stream) {
+  int kp = 16;
+  while (kp < k) kp <<= 1;
+  const dim3 grid(kRmseCooGroups), block(64 * kWavesPerGroup);
+#define BGMF_RC(KPV)                                                                           \
+  hipLaunchKernelGGL(k_rmse_coo<KPV>, grid, block, 0, stream, rows, cols, vals, nnz, U, V, k, \
+                     partials)
+  switch (kp) {
+    case 16: BGMF_RC(16); break;
+    case 32: BGMF_RC(32); break;
+    case 64: BGMF_RC(64); break;
+    case 128: BGMF_RC(128); break;
+    case 256: BGMF_RC(256); break;
+    default: return hipErrorInvalidValue;
+  }
+#undef BGMF_RC
+  hipLaunchKernelGGL(k_rmse_final, dim3(1), dim3(256), 0, stream, partials,
+                     (int64_t)rmse_coo_partials_count(), nnz, out);
   return hipGetLastError();
 }
 
