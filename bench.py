@@ -42,6 +42,12 @@ def parse():
     ap.add_argument("--passes", type=int, default=1,
                     help="GPU_STEPS: sweeps of each block per epoch (an epoch then makes "
                          "passes x nnz updates)")
+    ap.add_argument("--balanced-cuts", type=int, default=0, metavar="MAX_COLS",
+                    help="use nnz-balanced block boundaries (at most MAX_COLS columns per "
+                         "column-block) instead of the paper's equal blocks; 0 = equal blocks")
+    ap.add_argument("--variant-steps", type=int, default=3,
+                    help="after the timed region, also time this many epochs with nnz-balanced "
+                         "blocks (reported as a separate object; 0 disables)")
     ap.add_argument("--v-staging", type=int, default=0,
                     help="0 automatic, 1 V slice in LDS, 2 V in global memory")
     ap.add_argument("--xcd-remap", type=int, default=1)
@@ -188,6 +194,11 @@ def main():
     mdl.set_option(bgmf.BGMF_OPT_XCD_REMAP, args.xcd_remap)
     mdl.set_option(bgmf.BGMF_OPT_V_STAGING, args.v_staging)
     mdl.set_option(bgmf.BGMF_OPT_BLOCK_PASSES, args.passes)
+    if args.balanced_cuts > 0:
+        rc, cc = bgmf.bgmf_balanced_cuts(w.n, w.m, w.p, w.rows, w.cols, 65536, args.balanced_cuts)
+        mdl.set_cuts(rc, cc)
+        log(f"balanced cuts: widest row-block {int(np.diff(rc).max())}, widest column-block "
+            f"{int(np.diff(cc).max())}")
     mdl.set_factors(w.U0, w.V0)
     t0 = time.perf_counter()
     mdl.load_coo(w.rows, w.cols, w.vals)
@@ -245,6 +256,34 @@ def main():
         tr = json.load(open(args.traffic))
         if tr.get("sweep_source_sha1") == _sha1(SWEEP_SRC) and tr.get("nnz") == w.nnz:
             traffic = tr.get("bytes_per_launch")
+    variant = None
+    if args.variant_steps > 0 and args.balanced_cuts == 0:
+        # the same workload with nnz-balanced blocks (unequal block sizes, the
+        # paper's suggested extension): a separate measurement, never `value`
+        rc, cc = bgmf.bgmf_balanced_cuts(w.n, w.m, w.p, w.rows, w.cols, 65536, 64)
+        with bgmf.Model(w.n, w.m, w.k, w.p) as vm:
+            vm.set_stream(stream.cuda_stream)
+            vm.set_cuts(rc, cc)
+            vm.set_factors(w.U0, w.V0)
+            vm.load_coo(w.rows, w.cols, w.vals)
+            vchain = [int(x) for x in vm.chain_stats()]
+            vm.epoch(w.alpha, w.beta)
+            vm.rmse()
+            vs = []
+            for _ in range(args.variant_steps):
+                vm.epoch(w.alpha, w.beta)
+                vm.rmse()
+                vs.append(vm.timing())
+        v_sweep = float(np.mean([x[0] for x in vs]))
+        v_step = float(np.mean([x[0] + x[1] for x in vs]))
+        variant = {
+            "blocks": "nnz-balanced cut points (bgmf_balanced_cuts, at most 64 columns per "
+                      "column-block)",
+            "value": upd / (v_step / 1e3), "unit": "updates/s", "ms_per_step": v_step,
+            "sweep_ms": v_sweep, "roofline_frac": upd * b_alg / (v_sweep / 1e3) / 1e9 / HBM_PEAK_GBS,
+            "max_col_block": vchain[0], "max_row_block": vchain[1],
+        }
+        log(f"balanced blocks: sweep {v_sweep:.2f} ms, step {v_step:.2f} ms")
     cpu = cpu_baseline(w, args.cpu_seconds) if args.cpu_seconds > 0 else None
     out = {
         "metric": METRIC,
@@ -263,7 +302,9 @@ def main():
             "workload": (f"{args.config}: n={w.n} users, m={w.m} items, {nnz} ratings "
                          f"(lognormal user degree, Zipf(1.2) items), k={w.k}, p={w.p}, "
                          f"alpha={w.alpha}, beta={w.beta}; step = one epoch + RMSE pass"
-                         + (f"; {args.passes} passes per block" if args.passes > 1 else "")),
+                         + (f"; {args.passes} passes per block" if args.passes > 1 else "")
+                         + (f"; nnz-balanced blocks (at most {args.balanced_cuts} columns)"
+                            if args.balanced_cuts > 0 else "")),
             "sweep": kernel,
         },
         "roofline": {
@@ -277,6 +318,7 @@ def main():
             "bytes_per_update": b_alg,
         },
         "cpu_baseline": cpu,
+        "balanced_blocks_variant": variant,
         "sweep_ms": sweep_avg,
         "sweep_updates_per_s": upd / (sweep_avg / 1e3),
         "rmse_pass_ms": float(np.mean(rmse_ms)),

@@ -112,6 +112,35 @@ int bgmf_epoch(bgmf_t *h, float alpha, float beta);
  * stream. */
 int bgmf_rmse(bgmf_t *h, double *out);
 
+/* Block boundaries.  By default the grid has the paper's equal blocks
+ * (Eq. 4): row-block R holds rows [ceil(R n/p), ceil((R+1) n/p)), and the
+ * same for columns.  bgmf_set_cuts replaces them by caller-given cut points
+ * (row_cuts, col_cuts: p + 1 values each, host memory, strictly increasing
+ * from 0 to n, resp. m; row-blocks at most 65536 rows, column-blocks at most
+ * 16384 columns wide, else BGMF_E_ARG): row i is then in the block R with
+ * row_cuts[R] <= i < row_cuts[R+1].  Strata, the order inside a block and
+ * the update are unchanged.  Blocks of unequal size are the paper's
+ * suggested extension (Section 3); balanced blocks shorten the serial
+ * chains of skewed data.  Drops any loaded ratings (load them again).
+ * bgmf_get_cuts copies the cut points in effect (either pointer may be NULL). */
+int bgmf_set_cuts(bgmf_t *h, const int64_t *row_cuts, const int64_t *col_cuts);
+int bgmf_get_cuts(const bgmf_t *h, int64_t *row_cuts, int64_t *col_cuts);
+
+/* Cut points that balance the ratings over the blocks, from host COO arrays
+ * (no handle needed): for each dimension, block b (b = 0..p-2) ends at the
+ * first index where the running count of ratings reaches ceil(remaining /
+ * blocks left) — or just before that index if it alone holds that many, so
+ * that heavy rows and columns get blocks of their own — within 1 ..
+ * max_rows (max_cols) indices and leaving every later block at least one
+ * index and at most max_rows (max_cols).  Writes
+ * p + 1 values to each output.  Exact integer arithmetic.  BGMF_E_ARG if no
+ * such cuts exist (p > min(n, m), or p * max_rows < n, or p * max_cols < m);
+ * BGMF_E_RANGE for a rating outside the matrix.  Errors are reported by
+ * bgmf_last_error(NULL). */
+int bgmf_balanced_cuts(int64_t n, int64_t m, int32_t p, const int32_t *rows, const int32_t *cols,
+                       int64_t nnz, int64_t max_rows, int64_t max_cols, int64_t *row_cuts,
+                       int64_t *col_cuts);
+
 /* RMSE of the current factors over nnz caller-given ratings in host COO
  * arrays (for example a held-out split, the paper's Table 2 "test RMSE"):
  * sqrt((1/nnz) sum_e (vals[e] - u_rows[e].v_cols[e])^2), dots in fp32, sum

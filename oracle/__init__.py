@@ -11,6 +11,7 @@ pure-Python twin for tiny inputs.
 
 Functions follow the paper's Section 1:
   * ``bucket``   — the p x p block grid of Eq. 4 and the strata of Section 1.1
+  * ``bucket_cuts`` — the same with given (unequal) block boundaries
   * ``sgd_update`` — one per-rating step of Eq. 2-3 (Eq. 14-15 per element)
   * ``epoch`` / ``epoch_mt`` / ``epoch_ordered`` — one CPU step of
     Algorithm 1 with one pass per block
@@ -61,6 +62,8 @@ def _load():
         I64, I32, F32, F64 = ctypes.c_int64, ctypes.c_int32, ctypes.c_float, ctypes.c_double
         lib.oracle_bucket.argtypes = [I64, I64, I64, I64, i32p, i32p, i64p, i32p]
         lib.oracle_bucket.restype = ctypes.c_int
+        lib.oracle_bucket_cuts.argtypes = [I64, I64, I64, i64p, i64p, I64, i32p, i32p, i64p, i32p]
+        lib.oracle_bucket_cuts.restype = ctypes.c_int
         lib.oracle_sgd_update.argtypes = [I32, f32p, f32p, F32, F32, F32]
         lib.oracle_sgd_update.restype = None
         lib.oracle_sgd_update_f64.argtypes = [I32, f64p, f64p, F32, F32, F32]
@@ -105,6 +108,21 @@ def bucket(n: int, m: int, p: int, rows, cols):
     if rc != 0:
         raise MemoryError("oracle_bucket: out of memory")
     return block_ptr, perm[:nnz]
+
+
+def bucket_cuts(n: int, m: int, p: int, row_cuts, col_cuts, rows, cols):
+    """Bucketing with given block boundaries (p + 1 cut points per
+    dimension); returns (block_ptr, perm) as ``bucket``."""
+    rows = _c(rows, np.int32)
+    cols = _c(cols, np.int32)
+    nnz = rows.shape[0]
+    bp = np.zeros(p * p + 1, dtype=np.int64)
+    perm = np.zeros(max(nnz, 1), dtype=np.int32)
+    rc = _load().oracle_bucket_cuts(n, m, p, _c(row_cuts, np.int64), _c(col_cuts, np.int64), nnz,
+                                    rows, cols, bp, perm)
+    if rc != 0:
+        raise MemoryError("oracle_bucket_cuts: out of memory")
+    return bp, perm[:nnz]
 
 
 def sgd_update(u, v, x: float, alpha: float, beta: float):

@@ -94,6 +94,60 @@ int oracle_bucket(int64_t n, int64_t m, int64_t p, int64_t nnz,
     return 0;
 }
 
+/* Bucketing with given block boundaries (unequal blocks, the extension the
+ * paper suggests in Section 3): row-block R holds rows
+ * [row_cuts[R], row_cuts[R+1]), column-block C columns
+ * [col_cuts[C], col_cuts[C+1]); strata and slots as above.  With
+ * row_cuts[R] = ceil(R n / p) (and the same for columns) this is
+ * oracle_bucket. */
+static int64_t block_of_cut(const int64_t *cut, int64_t p, int64_t i)
+{
+    int64_t lo = 0, hi = p - 1;   /* the last R with cut[R] <= i */
+    while (lo < hi) {
+        int64_t mid = (lo + hi + 1) / 2;
+        if (cut[mid] <= i) lo = mid; else hi = mid - 1;
+    }
+    return lo;
+}
+
+static int64_t slot_of_cuts(int64_t i, int64_t j, int64_t p,
+                            const int64_t *row_cuts, const int64_t *col_cuts)
+{
+    int64_t R = block_of_cut(row_cuts, p, i);
+    int64_t C = block_of_cut(col_cuts, p, j);
+    int64_t s = ((C - R) % p + p) % p;
+    return s * p + R;
+}
+
+int oracle_bucket_cuts(int64_t n, int64_t m, int64_t p, const int64_t *row_cuts,
+                       const int64_t *col_cuts, int64_t nnz, const int32_t *rows,
+                       const int32_t *cols, int64_t *block_ptr, int32_t *perm)
+{
+    (void)m;
+    int64_t nslots = p * p;
+    int64_t *row_count = (int64_t *)calloc((size_t)n + 1, sizeof(int64_t));
+    int32_t *by_row = (int32_t *)malloc((size_t)(nnz > 0 ? nnz : 1) * sizeof(int32_t));
+    int64_t *slot_pos = (int64_t *)calloc((size_t)nslots + 1, sizeof(int64_t));
+    if (!row_count || !by_row || !slot_pos) {
+        free(row_count); free(by_row); free(slot_pos);
+        return -1;
+    }
+    for (int64_t e = 0; e < nnz; ++e) row_count[rows[e] + 1] += 1;
+    for (int64_t i = 0; i < n; ++i) row_count[i + 1] += row_count[i];
+    for (int64_t e = 0; e < nnz; ++e) by_row[row_count[rows[e]]++] = (int32_t)e;
+    for (int64_t q = 0; q <= nslots; ++q) block_ptr[q] = 0;
+    for (int64_t e = 0; e < nnz; ++e)
+        block_ptr[slot_of_cuts(rows[e], cols[e], p, row_cuts, col_cuts) + 1] += 1;
+    for (int64_t q = 0; q < nslots; ++q) block_ptr[q + 1] += block_ptr[q];
+    for (int64_t q = 0; q < nslots; ++q) slot_pos[q] = block_ptr[q];
+    for (int64_t t = 0; t < nnz; ++t) {
+        int32_t e = by_row[t];
+        perm[slot_pos[slot_of_cuts(rows[e], cols[e], p, row_cuts, col_cuts)]++] = e;
+    }
+    free(row_count); free(by_row); free(slot_pos);
+    return 0;
+}
+
 /* ---------------------------------------------------------------------- */
 /* One SGD step on one rating (Eq. 2-3; Eq. 14-15 per element).            */
 /* ---------------------------------------------------------------------- */

@@ -41,7 +41,8 @@ EXPORTED = (
     "bgmf_create", "bgmf_destroy", "bgmf_last_error", "bgmf_set_stream", "bgmf_set_factors",
     "bgmf_load_coo", "bgmf_epoch", "bgmf_rmse", "bgmf_get_factors", "bgmf_get_layout",
     "bgmf_sync", "bgmf_factor_ptrs", "bgmf_set_option", "bgmf_get_option", "bgmf_get_timing",
-    "bgmf_chain_stats", "bgmf_rmse_coo", "bgmf_fit",
+    "bgmf_chain_stats", "bgmf_rmse_coo", "bgmf_fit", "bgmf_set_cuts", "bgmf_get_cuts",
+    "bgmf_balanced_cuts",
 )
 
 
@@ -78,6 +79,9 @@ def _load() -> ctypes.CDLL:
         "bgmf_chain_stats": ([vp, vp], c_int),
         "bgmf_rmse_coo": ([vp, vp, vp, vp, I64, ctypes.POINTER(ctypes.c_double)], c_int),
         "bgmf_fit": ([vp, F32, F32, I32, ctypes.c_double, ctypes.POINTER(I32), vp], c_int),
+        "bgmf_set_cuts": ([vp, vp, vp], c_int),
+        "bgmf_get_cuts": ([vp, vp, vp], c_int),
+        "bgmf_balanced_cuts": ([I64, I64, I32, vp, vp, I64, I64, I64, vp, vp], c_int),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -222,6 +226,33 @@ def bgmf_fit(h, alpha: float, beta: float, max_epochs: int, delta: float):
     return ran.value, hist[: ran.value + 1]
 
 
+def bgmf_set_cuts(h, row_cuts, col_cuts) -> None:
+    r = np.ascontiguousarray(row_cuts, dtype=np.int64)
+    c = np.ascontiguousarray(col_cuts, dtype=np.int64)
+    _check(h, _lib.bgmf_set_cuts(h, _ptr(r), _ptr(c)))
+
+
+def bgmf_get_cuts(h, p: int):
+    r = np.empty(p + 1, dtype=np.int64)
+    c = np.empty(p + 1, dtype=np.int64)
+    _check(h, _lib.bgmf_get_cuts(h, _ptr(r), _ptr(c)))
+    return r, c
+
+
+def bgmf_balanced_cuts(n: int, m: int, p: int, rows, cols, max_rows: int = 65536,
+                       max_cols: int = 16384):
+    rows = np.ascontiguousarray(rows, dtype=np.int32)
+    cols = np.ascontiguousarray(cols, dtype=np.int32)
+    r = np.empty(p + 1, dtype=np.int64)
+    c = np.empty(p + 1, dtype=np.int64)
+    rc = _lib.bgmf_balanced_cuts(int(n), int(m), int(p), _ptr(rows), _ptr(cols), rows.shape[0],
+                                 int(max_rows), int(max_cols), _ptr(r), _ptr(c))
+    if rc != BGMF_OK:
+        msg = _lib.bgmf_last_error(None)
+        raise BgmfError(rc, msg.decode() if msg else "bgmf_balanced_cuts failed")
+    return r, c
+
+
 # --- convenience wrapper -----------------------------------------------------
 
 class Model:
@@ -291,3 +322,9 @@ class Model:
 
     def fit(self, alpha: float, beta: float, max_epochs: int, delta: float):
         return bgmf_fit(self.h, alpha, beta, max_epochs, delta)
+
+    def set_cuts(self, row_cuts, col_cuts):
+        bgmf_set_cuts(self.h, row_cuts, col_cuts)
+
+    def get_cuts(self):
+        return bgmf_get_cuts(self.h, self.p)

@@ -35,6 +35,10 @@ struct bgmf {
   double *partials = nullptr, *d_rmse = nullptr;
   int64_t epochs_done = 0;
   bool factors_set = false, loaded = false;
+  // block cut points (host copies and device tables, p + 1 each)
+  std::vector<int64_t> rcut, ccut;
+  int64_t *d_cuts = nullptr;  // rcut then ccut
+  int64_t rows_max = 0;
   // launch shapes: V slice staged in LDS (when it fits) and V in global memory
   int cols_max = 0;
   size_t lds_limit = 0;
@@ -141,6 +145,57 @@ int sync_checked(bgmf_t *h) {
   return check_device_error(h);
 }
 
+Grid grid_of(const bgmf_t *h) {
+  return Grid{h->n, h->m, h->p, h->d_cuts, h->d_cuts + h->p + 1};
+}
+
+// Launch shapes of the sweep for the current widest column-block: the widest
+// workgroup (4, 2 or 1 waves) whose LDS column slices fit, whether all p
+// waves can be resident at once (persistent schedule) for the LDS and the
+// global-memory placements.  The kernels' dynamic-LDS limit is set to the
+// device's, the most any handle may ask for.
+hipError_t configure_sweep(bgmf_t *h) {
+  const bool mask = h->k != h->kp;
+  const int64_t p = h->p;
+  int per_cu = 0;
+  hipError_t e;
+  for (int vm : {kVLds, kVGlobal, kVGlobalCoherent})
+    if ((e = sgd_set_lds_limit(h->kp, mask, vm, h->lds_limit)) != hipSuccess) return e;
+  const size_t slice = (size_t)(h->cols_max + 1) * h->kp * sizeof(float);
+  h->wpg_lds = kWavesPerGroup;
+  while (h->wpg_lds > 1 && h->wpg_lds * slice > h->lds_limit) h->wpg_lds >>= 1;
+  h->lds_bytes_lds = h->wpg_lds * slice;
+  h->lds_fits = h->lds_bytes_lds <= h->lds_limit;
+  h->coop_lds = false;
+  if (h->lds_fits) {
+    if ((e = sgd_occupancy(h->kp, mask, kVLds, h->wpg_lds, h->lds_bytes_lds, &per_cu)) !=
+        hipSuccess)
+      return e;
+    h->coop_lds = (int64_t)per_cu * h->cus >= (p + h->wpg_lds - 1) / h->wpg_lds;
+  }
+  h->wpg_gv = kWavesPerGroup;
+  h->lds_bytes_gv = h->wpg_gv * sgd_gv_lds_per_wave(h->kp);
+  if ((e = sgd_occupancy(h->kp, mask, kVGlobalCoherent, h->wpg_gv, h->lds_bytes_gv, &per_cu)) !=
+      hipSuccess)
+    return e;
+  h->coop_gv = (int64_t)per_cu * h->cus >= (p + h->wpg_gv - 1) / h->wpg_gv;
+  if (h->v_staging == 1 && !h->lds_fits) h->v_staging = 0;
+  return hipSuccess;
+}
+
+// Host check of cut points: p + 1 strictly increasing values from 0 to len,
+// each block at most max_width wide.  Returns the widest block, or -1.
+int64_t check_cuts(const int64_t *cut, int32_t p, int64_t len, int64_t max_width) {
+  if (cut[0] != 0 || cut[p] != len) return -1;
+  int64_t widest = 0;
+  for (int32_t b = 0; b < p; ++b) {
+    const int64_t w = cut[b + 1] - cut[b];
+    if (w < 1 || w > max_width) return -1;
+    widest = std::max(widest, w);
+  }
+  return widest;
+}
+
 }  // namespace
 
 extern "C" {
@@ -175,9 +230,14 @@ bgmf_t *bgmf_create(int64_t n, int64_t m, int32_t k, int32_t p) {
   h->p = p;
   h->kp = 16;
   while (h->kp < k) h->kp <<= 1;
-  const Grid G{n, m, p};
-  for (int64_t C = 0; C < p; ++C)
-    h->cols_max = std::max<int>(h->cols_max, (int)(G.col_start(C + 1) - G.col_start(C)));
+  h->rcut.resize((size_t)p + 1);
+  h->ccut.resize((size_t)p + 1);
+  for (int64_t b = 0; b <= p; ++b) {
+    h->rcut[b] = equal_cut(b, n, p);
+    h->ccut[b] = equal_cut(b, m, p);
+  }
+  h->rows_max = check_cuts(h->rcut.data(), p, n, 65536);
+  h->cols_max = (int)check_cuts(h->ccut.data(), p, m, 1 << kColBits);
 
   auto bail = [&](hipError_t e, const char *what) -> bgmf_t * {
     fail(nullptr, e == hipErrorOutOfMemory ? BGMF_E_NOMEM : BGMF_E_HIP, "%s: %s", what,
@@ -195,33 +255,14 @@ bgmf_t *bgmf_create(int64_t n, int64_t m, int32_t k, int32_t p) {
       hipSuccess)
     return bail(e, "hipDeviceGetAttribute");
   h->lds_limit = (size_t)lds_max;
-  // V slice in LDS: the widest workgroup (4, 2 or 1 waves) whose column
-  // slices fit; the persistent schedule needs all p waves resident at once
-  const bool mask = h->k != h->kp;
-  int per_cu = 0;
-  const size_t slice = (size_t)(h->cols_max + 1) * h->kp * sizeof(float);
-  h->wpg_lds = kWavesPerGroup;
-  while (h->wpg_lds > 1 && h->wpg_lds * slice > h->lds_limit) h->wpg_lds >>= 1;
-  h->lds_bytes_lds = h->wpg_lds * slice;
-  h->lds_fits = h->lds_bytes_lds <= h->lds_limit;
-  if (h->lds_fits) {
-    if ((e = sgd_set_lds_limit(h->kp, mask, kVLds, h->lds_bytes_lds)) != hipSuccess)
-      return bail(e, "hipFuncSetAttribute");
-    if ((e = sgd_occupancy(h->kp, mask, kVLds, h->wpg_lds, h->lds_bytes_lds, &per_cu)) !=
-        hipSuccess)
-      return bail(e, "hipOccupancyMaxActiveBlocksPerMultiprocessor");
-    h->coop_lds = (int64_t)per_cu * h->cus >= (p + h->wpg_lds - 1) / h->wpg_lds;
-  }
-  // V in global memory: only a ring of recent results per wave in LDS
-  h->wpg_gv = kWavesPerGroup;
-  h->lds_bytes_gv = h->wpg_gv * sgd_gv_lds_per_wave(h->kp);
-  for (int vm : {kVGlobal, kVGlobalCoherent})
-    if ((e = sgd_set_lds_limit(h->kp, mask, vm, h->lds_bytes_gv)) != hipSuccess)
-      return bail(e, "hipFuncSetAttribute");
-  if ((e = sgd_occupancy(h->kp, mask, kVGlobalCoherent, h->wpg_gv, h->lds_bytes_gv, &per_cu)) !=
-      hipSuccess)
-    return bail(e, "hipOccupancyMaxActiveBlocksPerMultiprocessor");
-  h->coop_gv = (int64_t)per_cu * h->cus >= (p + h->wpg_gv - 1) / h->wpg_gv;
+  if ((e = configure_sweep(h)) != hipSuccess) return bail(e, "configure_sweep");
+  if ((e = hipMalloc(&h->d_cuts, 2 * ((size_t)p + 1) * sizeof(int64_t))) != hipSuccess)
+    return bail(e, "hipMalloc(cuts)");
+  if ((e = hipMemcpy(h->d_cuts, h->rcut.data(), ((size_t)p + 1) * sizeof(int64_t),
+                     hipMemcpyHostToDevice)) != hipSuccess ||
+      (e = hipMemcpy(h->d_cuts + p + 1, h->ccut.data(), ((size_t)p + 1) * sizeof(int64_t),
+                     hipMemcpyHostToDevice)) != hipSuccess)
+    return bail(e, "hipMemcpy(cuts)");
   if ((e = hipStreamCreateWithFlags(&h->own_stream, hipStreamNonBlocking)) != hipSuccess)
     return bail(e, "hipStreamCreate");
   h->stream = h->own_stream;
@@ -259,6 +300,7 @@ void bgmf_destroy(bgmf_t *h) {
   hipFree(h->err);
   hipFree(h->partials);
   hipFree(h->d_rmse);
+  hipFree(h->d_cuts);
   for (auto &ev : h->ev)
     if (ev) hipEventDestroy(ev);
   if (h->own_stream) hipStreamDestroy(h->own_stream);
@@ -355,8 +397,8 @@ int bgmf_load_coo(bgmf_t *h, const int32_t *rows, const int32_t *cols, const flo
   // ratings that do not fit the budget are kept stratum-major, so that each
   // stratum is one contiguous range to stream
   const bool ooc = h->budget > 0 && (nnz + kRecPad) * (int64_t)sizeof(uint2) > h->budget;
-  LOAD_TRY(bucket(d_rows, d_cols, d_vals, nnz, h->n, h->m, h->p, ooc, scratch, scratch_bytes, out,
-                  h->err, h->stream));
+  LOAD_TRY(bucket(d_rows, d_cols, d_vals, nnz, grid_of(h), h->rows_max, ooc, scratch,
+                  scratch_bytes, out, h->err, h->stream));
   LOAD_TRY(hipStreamSynchronize(h->stream));
   cleanup();
 #undef LOAD_TRY
@@ -576,6 +618,8 @@ int bgmf_epoch(bgmf_t *h, float alpha, float beta) {
   P.err = h->err;
   P.n = h->n;
   P.m = h->m;
+  P.rcut = h->d_cuts;
+  P.ccut = h->d_cuts + h->p + 1;
   P.k = h->k;
   P.p = h->p;
   P.cols_max = h->cols_max;
@@ -650,8 +694,8 @@ int bgmf_rmse(bgmf_t *h, double *out) {
     int rc = stream_begin(h);
     if (rc != BGMF_OK) return rc;
     if (h->s_res > 0)
-      HIP_TRY(h, rmse_stratum_add(h->resident, 0, h->block_ptr, 0, h->s_res, h->U, h->V, h->n,
-                                  h->m, h->k, h->p, h->partials, h->stream));
+      HIP_TRY(h, rmse_stratum_add(h->resident, 0, h->block_ptr, 0, h->s_res, h->U, h->V,
+                                  grid_of(h), h->k, h->partials, h->stream));
     for (size_t c = 0; c + 1 < h->chunk.size(); ++c) {
       const int32_t s0 = h->chunk[c], s1 = h->chunk[c + 1];
       const uint2 *slot_rec = nullptr;
@@ -659,14 +703,14 @@ int bgmf_rmse(bgmf_t *h, double *out) {
       if (rc != BGMF_OK) return rc;
       if (h->strat[s1] > h->strat[s0])
         HIP_TRY(h, rmse_stratum_add(slot_rec, h->strat[s0], h->block_ptr, s0, s1, h->U, h->V,
-                                    h->n, h->m, h->k, h->p, h->partials, h->stream));
+                                    grid_of(h), h->k, h->partials, h->stream));
       rc = chunk_done(h, c);
       if (rc != BGMF_OK) return rc;
     }
     HIP_TRY(h, rmse_stratum_end(h->partials, h->p, h->nnz, h->d_rmse, h->stream));
   } else {
-    HIP_TRY(h, launch_rmse(h->rec, h->wblock_ptr, h->U, h->V, h->n, h->m, h->k, h->p, h->nnz,
-                           h->partials, h->d_rmse, h->lds_limit, h->stream));
+    HIP_TRY(h, launch_rmse(h->rec, h->wblock_ptr, h->U, h->V, grid_of(h), h->rows_max, h->k,
+                           h->nnz, h->partials, h->d_rmse, h->lds_limit, h->stream));
   }
   HIP_TRY(h, hipEventRecord(h->ev[3], h->stream));
   h->rmse_timed = true;
@@ -675,6 +719,100 @@ int bgmf_rmse(bgmf_t *h, double *out) {
   int rc = sync_checked(h);
   if (rc != BGMF_OK) return rc;
   *out = r;
+  return BGMF_OK;
+}
+
+namespace {
+
+// Greedy nnz-balanced cut points over one dimension of length len: block b
+// ends at the first index where the running count of ratings reaches its
+// share of what is left (ceil(remaining / blocks left)); if that last index
+// alone holds a full share, the block ends before it instead, so that heavy
+// rows or columns get blocks of their own (one index cannot be split, and
+// its ratings form one serial chain).  Blocks stay at least one and at most
+// cap wide, leaving every later block at least one index and at most cap.
+// Integer arithmetic only, so the result is exact.
+bool balanced_dim(const std::vector<int64_t> &deg, int32_t p, int64_t cap, int64_t *cut) {
+  const int64_t len = (int64_t)deg.size();
+  if (p < 1 || p > len || cap < 1 || cap * p < len) return false;
+  std::vector<int64_t> cum((size_t)len + 1, 0);
+  for (int64_t i = 0; i < len; ++i) cum[i + 1] = cum[i] + deg[i];
+  const int64_t total = cum[len];
+  cut[0] = 0;
+  for (int32_t b = 1; b < p; ++b) {
+    const int64_t prev = cut[b - 1];
+    const int64_t left = p - b + 1;  // blocks b-1 .. p-1
+    const int64_t target = cum[prev] + (total - cum[prev] + left - 1) / left;
+    int64_t c = (int64_t)(std::lower_bound(cum.begin() + prev + 1, cum.end(), target) -
+                          cum.begin());
+    if (c <= len && c - 1 > prev && deg[c - 1] >= target - cum[prev]) c -= 1;
+    c = std::max(c, prev + 1);
+    c = std::min(c, prev + cap);
+    c = std::min(c, len - (p - b));                      // one index for each later block
+    c = std::max(c, len - (int64_t)(p - b) * cap);       // later blocks within the cap
+    cut[b] = c;
+  }
+  cut[p] = len;
+  return true;
+}
+
+}  // namespace
+
+int bgmf_balanced_cuts(int64_t n, int64_t m, int32_t p, const int32_t *rows, const int32_t *cols,
+                       int64_t nnz, int64_t max_rows, int64_t max_cols, int64_t *row_cuts,
+                       int64_t *col_cuts) {
+  if (!rows || !cols || !row_cuts || !col_cuts || nnz < 0 || n < 1 || m < 1) {
+    fail(nullptr, BGMF_E_ARG, "bgmf_balanced_cuts: bad arguments");
+    return BGMF_E_ARG;
+  }
+  max_rows = std::min<int64_t>(max_rows, 65536);
+  max_cols = std::min<int64_t>(max_cols, 1 << kColBits);
+  std::vector<int64_t> rd((size_t)n, 0), cd((size_t)m, 0);
+  for (int64_t e = 0; e < nnz; ++e) {
+    if (rows[e] < 0 || rows[e] >= n || cols[e] < 0 || cols[e] >= m) {
+      fail(nullptr, BGMF_E_RANGE, "rating %lld at (%d, %d) is outside the %lld x %lld matrix",
+           (long long)e, rows[e], cols[e], (long long)n, (long long)m);
+      return BGMF_E_RANGE;
+    }
+    rd[rows[e]] += 1;
+    cd[cols[e]] += 1;
+  }
+  if (!balanced_dim(rd, p, max_rows, row_cuts) || !balanced_dim(cd, p, max_cols, col_cuts)) {
+    fail(nullptr, BGMF_E_ARG,
+         "no cut points: need 1 <= p <= min(n, m), p * max_rows >= n and p * max_cols >= m");
+    return BGMF_E_ARG;
+  }
+  return BGMF_OK;
+}
+
+int bgmf_set_cuts(bgmf_t *h, const int64_t *row_cuts, const int64_t *col_cuts) {
+  if (!h) return BGMF_E_ARG;
+  if (!row_cuts || !col_cuts) return fail(h, BGMF_E_ARG, "bgmf_set_cuts: null pointer");
+  const int64_t rmax = check_cuts(row_cuts, h->p, h->n, 65536);
+  const int64_t cmax = check_cuts(col_cuts, h->p, h->m, 1 << kColBits);
+  if (rmax < 0 || cmax < 0)
+    return fail(h, BGMF_E_ARG,
+                "cut points must rise strictly from 0 to n (rows, blocks at most 65536 wide) and "
+                "from 0 to m (columns, blocks at most %d wide)",
+                1 << kColBits);
+  HIP_TRY(h, hipStreamSynchronize(h->stream));
+  free_layout(h);
+  h->rcut.assign(row_cuts, row_cuts + h->p + 1);
+  h->ccut.assign(col_cuts, col_cuts + h->p + 1);
+  h->rows_max = rmax;
+  h->cols_max = (int)cmax;
+  HIP_TRY(h, configure_sweep(h));
+  HIP_TRY(h, hipMemcpy(h->d_cuts, h->rcut.data(), ((size_t)h->p + 1) * sizeof(int64_t),
+                       hipMemcpyHostToDevice));
+  HIP_TRY(h, hipMemcpy(h->d_cuts + h->p + 1, h->ccut.data(), ((size_t)h->p + 1) * sizeof(int64_t),
+                       hipMemcpyHostToDevice));
+  return BGMF_OK;
+}
+
+int bgmf_get_cuts(const bgmf_t *h, int64_t *row_cuts, int64_t *col_cuts) {
+  if (!h) return BGMF_E_ARG;
+  if (row_cuts) std::memcpy(row_cuts, h->rcut.data(), ((size_t)h->p + 1) * sizeof(int64_t));
+  if (col_cuts) std::memcpy(col_cuts, h->ccut.data(), ((size_t)h->p + 1) * sizeof(int64_t));
   return BGMF_OK;
 }
 

@@ -38,8 +38,8 @@ __global__ void k_make_keys(const int32_t *__restrict__ rows, const int32_t *__r
                             int32_t *__restrict__ idx) {
   for (int64_t e = gid(); e < nnz; e += (int64_t)gridDim.x * blockDim.x) {
     const int64_t i = rows[e], j = cols[e];
-    const int64_t R = (i * G.p) / G.n;
-    const int64_t C = (j * G.p) / G.m;
+    const int64_t R = G.row_block(i);
+    const int64_t C = G.col_block(j);
     int64_t s = C - R;
     if (s < 0) s += G.p;
     const uint64_t q = (uint64_t)(s * G.p + R);
@@ -305,15 +305,10 @@ size_t bucket_scratch_bytes(int64_t nnz, int32_t p) {
 }
 
 hipError_t bucket(const int32_t *rows, const int32_t *cols, const float *vals, int64_t nnz,
-                  int64_t n, int64_t m, int32_t p, bool stratum_major, void *scratch,
+                  const Grid &G, int64_t rows_max, bool stratum_major, void *scratch,
                   size_t scratch_bytes, const BucketOut &out, int32_t *err, hipStream_t st) {
-  Grid G{n, m, p};
+  const int32_t p = G.p;
   const int64_t slots = (int64_t)p * p;
-  int64_t rows_max = 0;
-  for (int64_t R = 0; R < p; ++R) {
-    const int64_t w = G.row_start(R + 1) - G.row_start(R);
-    if (w > rows_max) rows_max = w;
-  }
   const int rbits = bits_for((uint64_t)(rows_max < 1 ? 1 : rows_max));
   const int qbits = bits_for((uint64_t)slots);
   const int total_bits = rbits + qbits;

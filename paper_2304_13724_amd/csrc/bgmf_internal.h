@@ -23,17 +23,33 @@ constexpr uint32_t kColMask = (1u << kColBits) - 1u;
 constexpr int kPrefetch = BGMF_PREFETCH;     // prefetch distance of factor rows (ratings)
 constexpr int kRecPad = 256;                 // padding records after the last stream
 
-// Block geometry of the p x p grid: row-block R holds rows
-// [ceil(R n / p), ceil((R+1) n / p)), i.e. row i is in floor(i p / n).
+// Block geometry of the p x p grid, as cut points: row-block R holds rows
+// [rcut[R], rcut[R+1]), column-block C columns [ccut[C], ccut[C+1]) (p + 1
+// strictly increasing values from 0 to n, resp. m, in device memory).  The
+// paper's equal blocks (Eq. 4) are rcut[R] = ceil(R n / p), i.e. row i in
+// block floor(i p / n); other cut points give blocks of unequal size.
+__host__ __device__ __forceinline__ int64_t equal_cut(int64_t R, int64_t n, int32_t p) {
+  return (R * n + p - 1) / p;
+}
+
+__device__ __forceinline__ int32_t block_of(const int64_t *cut, int32_t p, int64_t i) {
+  int32_t lo = 0, hi = p - 1;  // the last R with cut[R] <= i
+  while (lo < hi) {
+    const int32_t mid = (lo + hi + 1) >> 1;
+    if (cut[mid] <= i) lo = mid;
+    else hi = mid - 1;
+  }
+  return lo;
+}
+
 struct Grid {
   int64_t n, m;
   int32_t p;
-  __host__ __device__ __forceinline__ int64_t row_start(int64_t R) const {
-    return (R * n + p - 1) / p;
-  }
-  __host__ __device__ __forceinline__ int64_t col_start(int64_t C) const {
-    return (C * m + p - 1) / p;
-  }
+  const int64_t *rcut, *ccut;
+  __device__ __forceinline__ int64_t row_start(int64_t R) const { return rcut[R]; }
+  __device__ __forceinline__ int64_t col_start(int64_t C) const { return ccut[C]; }
+  __device__ __forceinline__ int32_t row_block(int64_t i) const { return block_of(rcut, p, i); }
+  __device__ __forceinline__ int32_t col_block(int64_t j) const { return block_of(ccut, p, j); }
 };
 
 // Arguments of the SGD sweep kernels.
@@ -48,6 +64,7 @@ struct SgdParams {
   int64_t *flags;            // [p * kFlagStride]: strata completed by each row-block
   int32_t *err;              // device error word (0 = ok)
   int64_t n, m;
+  const int64_t *rcut, *ccut;  // block cut points (see Grid)
   int32_t k, p;
   int32_t cols_max;          // largest column-block width
   int32_t s_begin, s_end;    // strata of this launch
@@ -79,7 +96,7 @@ hipError_t sgd_set_lds_limit(int kp, bool mask, int vmode, size_t lds_bytes);
 size_t sgd_gv_lds_per_wave(int kp);
 
 hipError_t launch_rmse(const uint2 *rec, const int64_t *wblock_ptr, const float *U,
-                       const float *V, int64_t n, int64_t m, int32_t k, int32_t p, int64_t nnz,
+                       const float *V, const Grid &G, int64_t rows_max, int32_t k, int64_t nnz,
                        double *partials, double *out, size_t lds_limit, hipStream_t stream);
 // Out-of-core pieces of the RMSE pass: zero the partial sums
 // (kRmseStrataGroups per row-block), add the squared errors of strata
@@ -88,9 +105,8 @@ hipError_t launch_rmse(const uint2 *rec, const int64_t *wblock_ptr, const float 
 constexpr int kRmseStrataGroups = 16;
 hipError_t rmse_stratum_begin(double *partials, int32_t p, hipStream_t stream);
 hipError_t rmse_stratum_add(const uint2 *rec, int64_t rec_origin, const int64_t *block_ptr,
-                            int32_t s0, int32_t s1, const float *U, const float *V, int64_t n,
-                            int64_t m, int32_t k, int32_t p, double *partials,
-                            hipStream_t stream);
+                            int32_t s0, int32_t s1, const float *U, const float *V,
+                            const Grid &G, int32_t k, double *partials, hipStream_t stream);
 hipError_t rmse_stratum_end(const double *partials, int32_t p, int64_t nnz, double *out,
                             hipStream_t stream);
 size_t rmse_partials_count(int32_t p);
@@ -113,8 +129,9 @@ struct BucketOut {
 size_t bucket_scratch_bytes(int64_t nnz, int32_t p);
 // stratum_major: records in slot order (each stratum contiguous) instead of
 // wave-major order.
+// rows_max: the widest row-block (sets the key width).
 hipError_t bucket(const int32_t *rows, const int32_t *cols, const float *vals, int64_t nnz,
-                  int64_t n, int64_t m, int32_t p, bool stratum_major, void *scratch,
+                  const Grid &G, int64_t rows_max, bool stratum_major, void *scratch,
                   size_t scratch_bytes, const BucketOut &out, int32_t *err, hipStream_t stream);
 
 }  // namespace bgmfk

@@ -24,8 +24,9 @@ __device__ __forceinline__ float dpp_mov(float x) {
 template <int KP>
 __global__ void __launch_bounds__(256)
 k_rmse_partial(const uint2 *__restrict__ rec, const int64_t *__restrict__ wblock_ptr,
-               const float *__restrict__ U, const float *__restrict__ V, int64_t n, int64_t m,
-               int32_t k, int32_t p, double *__restrict__ partials) {
+               const float *__restrict__ U, const float *__restrict__ V, Grid G, int32_t k,
+               double *__restrict__ partials) {
+  const int32_t p = G.p;
   constexpr int L = KP >= 64 ? 16 : KP / 4;  // lanes per rating
   constexpr int RPS = 64 / L;                // ratings per wave step
   constexpr int Q = KP / 4;                  // float4 slices per padded row
@@ -35,7 +36,6 @@ k_rmse_partial(const uint2 *__restrict__ rec, const int64_t *__restrict__ wblock
   const int gl = lane % L, grp = lane / L;
   const int b = blockIdx.x / kRmseSplit;          // row-block
   const int w0 = (blockIdx.x % kRmseSplit) * kWavesPerGroup + wave;  // first stratum
-  const Grid G{n, m, p};
   const float *Ub = U + G.row_start(b) * k;
   const uint32_t rmax = (uint32_t)(G.row_start(b + 1) - G.row_start(b)) - 1u;
   const int kq = k / 4;
@@ -118,8 +118,9 @@ template <int KP>
 __global__ void __launch_bounds__(256)
 k_rmse_stratum(const uint2 *__restrict__ rec, int64_t rec_origin,
                const int64_t *__restrict__ block_ptr, int32_t s0, int32_t s1,
-               const float *__restrict__ U, const float *__restrict__ V, int64_t n, int64_t m,
-               int32_t k, int32_t p, double *__restrict__ partials) {
+               const float *__restrict__ U, const float *__restrict__ V, Grid G, int32_t k,
+               double *__restrict__ partials) {
+  const int32_t p = G.p;
   constexpr int L = KP >= 64 ? 16 : KP / 4;
   constexpr int RPS = 64 / L;
   constexpr int Q = KP / 4;
@@ -129,7 +130,6 @@ k_rmse_stratum(const uint2 *__restrict__ rec, int64_t rec_origin,
   const int gl = lane % L, grp = lane / L;
   const int b = blockIdx.x * kWavesPerGroup + wave;
   if (b >= p) return;
-  const Grid G{n, m, p};
   const float *Ub = U + G.row_start(b) * k;
   const uint32_t rmax = (uint32_t)(G.row_start(b + 1) - G.row_start(b)) - 1u;
   const int kq = k / 4;
@@ -247,8 +247,9 @@ constexpr int kLdsWaves = 16;
 template <int KP>
 __global__ void __launch_bounds__(1024)
 k_rmse_lds(const uint2 *__restrict__ rec, const int64_t *__restrict__ wblock_ptr,
-           const float *__restrict__ U, const float *__restrict__ V, int64_t n, int64_t m,
-           int32_t k, int32_t p, double *__restrict__ partials) {
+           const float *__restrict__ U, const float *__restrict__ V, Grid G, int32_t k,
+           double *__restrict__ partials) {
+  const int32_t p = G.p;
   constexpr int L = KP >= 64 ? 16 : KP / 4;
   constexpr int RPS = 64 / L;
   constexpr int Q = KP / 4;
@@ -258,7 +259,6 @@ k_rmse_lds(const uint2 *__restrict__ rec, const int64_t *__restrict__ wblock_ptr
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int gl = lane % L, grp = lane / L;
   const int b = blockIdx.x;
-  const Grid G{n, m, p};
   const int64_t r0 = G.row_start(b);
   const uint32_t rows_b = (uint32_t)(G.row_start(b + 1) - r0);
   const uint32_t rmax = rows_b - 1u;
@@ -359,12 +359,10 @@ size_t rmse_partials_count(int32_t p) {
 namespace {
 template <int KP>
 hipError_t launch_rmse_kp(const uint2 *rec, const int64_t *wblock_ptr, const float *U,
-                          const float *V, int64_t n, int64_t m, int32_t k, int32_t p,
+                          const float *V, const Grid &G, int64_t rows_max, int32_t k,
                           double *partials, size_t lds_limit, int64_t *count,
                           hipStream_t stream) {
-  const Grid G{n, m, p};
-  int64_t rows_max = 0;
-  for (int64_t R = 0; R < p; ++R) rows_max = std::max(rows_max, G.row_start(R + 1) - G.row_start(R));
+  const int32_t p = G.p;
   const size_t lds = (size_t)rows_max * (size_t)k * sizeof(float);
   if (lds <= lds_limit) {
     static bool attr_set = false;
@@ -376,11 +374,11 @@ hipError_t launch_rmse_kp(const uint2 *rec, const int64_t *wblock_ptr, const flo
       attr_set = true;
     }
     hipLaunchKernelGGL(k_rmse_lds<KP>, dim3((unsigned)p), dim3(64 * kLdsWaves), lds, stream, rec,
-                       wblock_ptr, U, V, n, m, k, p, partials);
+                       wblock_ptr, U, V, G, k, partials);
     *count = (int64_t)p * kLdsWaves;
   } else {
     hipLaunchKernelGGL(k_rmse_partial<KP>, dim3((unsigned)(p * kRmseSplit)), dim3(256), 0, stream,
-                       rec, wblock_ptr, U, V, n, m, k, p, partials);
+                       rec, wblock_ptr, U, V, G, k, partials);
     *count = (int64_t)p * kRmseSplit * kWavesPerGroup;
   }
   return hipGetLastError();
@@ -395,9 +393,9 @@ hipError_t rmse_stratum_begin(double *partials, int32_t p, hipStream_t stream) {
 }
 
 hipError_t rmse_stratum_add(const uint2 *rec, int64_t rec_origin, const int64_t *block_ptr,
-                            int32_t s0, int32_t s1, const float *U, const float *V, int64_t n,
-                            int64_t m, int32_t k, int32_t p, double *partials,
-                            hipStream_t stream) {
+                            int32_t s0, int32_t s1, const float *U, const float *V,
+                            const Grid &G, int32_t k, double *partials, hipStream_t stream) {
+  const int32_t p = G.p;
   int kp = 16;
   while (kp < k) kp <<= 1;
   const dim3 grid((unsigned)((p + kWavesPerGroup - 1) / kWavesPerGroup),
@@ -405,7 +403,7 @@ hipError_t rmse_stratum_add(const uint2 *rec, int64_t rec_origin, const int64_t 
       block(256);
 #define BGMF_RS(KPV)                                                                            \
   hipLaunchKernelGGL(k_rmse_stratum<KPV>, grid, block, 0, stream, rec, rec_origin, block_ptr, s0, \
-                     s1, U, V, n, m, k, p, partials)
+                     s1, U, V, G, k, partials)
   switch (kp) {
     case 16: BGMF_RS(16); break;
     case 32: BGMF_RS(32); break;
@@ -451,18 +449,18 @@ hipError_t launch_rmse_coo(const int32_t *rows, const int32_t *cols, const float
 }
 
 hipError_t launch_rmse(const uint2 *rec, const int64_t *wblock_ptr, const float *U,
-                       const float *V, int64_t n, int64_t m, int32_t k, int32_t p, int64_t nnz,
+                       const float *V, const Grid &G, int64_t rows_max, int32_t k, int64_t nnz,
                        double *partials, double *out, size_t lds_limit, hipStream_t stream) {
   int kp = 16;
   while (kp < k) kp <<= 1;
   int64_t count = 0;
   hipError_t e;
   switch (kp) {
-    case 16: e = launch_rmse_kp<16>(rec, wblock_ptr, U, V, n, m, k, p, partials, lds_limit, &count, stream); break;
-    case 32: e = launch_rmse_kp<32>(rec, wblock_ptr, U, V, n, m, k, p, partials, lds_limit, &count, stream); break;
-    case 64: e = launch_rmse_kp<64>(rec, wblock_ptr, U, V, n, m, k, p, partials, lds_limit, &count, stream); break;
-    case 128: e = launch_rmse_kp<128>(rec, wblock_ptr, U, V, n, m, k, p, partials, lds_limit, &count, stream); break;
-    case 256: e = launch_rmse_kp<256>(rec, wblock_ptr, U, V, n, m, k, p, partials, lds_limit, &count, stream); break;
+    case 16: e = launch_rmse_kp<16>(rec, wblock_ptr, U, V, G, rows_max, k, partials, lds_limit, &count, stream); break;
+    case 32: e = launch_rmse_kp<32>(rec, wblock_ptr, U, V, G, rows_max, k, partials, lds_limit, &count, stream); break;
+    case 64: e = launch_rmse_kp<64>(rec, wblock_ptr, U, V, G, rows_max, k, partials, lds_limit, &count, stream); break;
+    case 128: e = launch_rmse_kp<128>(rec, wblock_ptr, U, V, G, rows_max, k, partials, lds_limit, &count, stream); break;
+    case 256: e = launch_rmse_kp<256>(rec, wblock_ptr, U, V, G, rows_max, k, partials, lds_limit, &count, stream); break;
     default: return hipErrorInvalidValue;
   }
   if (e != hipSuccess) return e;

@@ -231,7 +231,7 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
   const uint32_t doff = ln.doff;
 
   extern __shared__ float lds[];
-  const Grid G{P.n, P.m, P.p};
+  const Grid G{P.n, P.m, P.p, P.rcut, P.ccut};
   const int k = P.k;
   const uint32_t rowbytes = (uint32_t)k * 4u;
   const uint32_t colbytes = (uint32_t)KP * 4u;
@@ -455,7 +455,7 @@ __global__ void __launch_bounds__(256) k_sgd_gv(SgdParams P) {
   const uint32_t doff = ln.doff;
 
   extern __shared__ float lds[];
-  const Grid G{P.n, P.m, P.p};
+  const Grid G{P.n, P.m, P.p, P.rcut, P.ccut};
   const int k = P.k;
   const uint32_t rowbytes = (uint32_t)k * 4u;
   const uint32_t slotbytes = (uint32_t)KP * 4u;

@@ -60,6 +60,39 @@ def test_bucket_brute_force(n, m, nnz, p, seed, distinct):
     assert np.array_equal(perm, perm_ref)
 
 
+def _equal_cuts(length, p):
+    return np.array([(R * length + p - 1) // p for R in range(p + 1)], dtype=np.int64)
+
+
+@pytest.mark.parametrize("n,m,nnz,p,seed", [(17, 11, 120, 3, 31), (40, 9, 300, 4, 32),
+                                             (1003, 997, 40_000, 13, 33)])
+def test_bucket_cuts_with_equal_cuts_is_bucket(n, m, nnz, p, seed):
+    rows, cols, _, _, _ = _small(n, m, nnz, 16, p, seed)
+    a = oracle.bucket(n, m, p, rows, cols)
+    b = oracle.bucket_cuts(n, m, p, _equal_cuts(n, p), _equal_cuts(m, p), rows, cols)
+    assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
+
+
+@pytest.mark.parametrize("seed", [41, 42, 43])
+def test_bucket_cuts_brute_force(seed):
+    """Random unequal cut points: slots and order from Python's sorted()."""
+    import bisect
+    rng = np.random.default_rng(seed)
+    n, m, p, nnz = 30, 25, 4, 200
+    rows, cols, _, _, _ = _small(n, m, nnz, 16, p, seed)
+    rc = np.r_[0, np.sort(rng.choice(np.arange(1, n), p - 1, replace=False)), n]
+    cc = np.r_[0, np.sort(rng.choice(np.arange(1, m), p - 1, replace=False)), m]
+    def slot(e):
+        R = bisect.bisect_right(rc.tolist(), int(rows[e])) - 1
+        C = bisect.bisect_right(cc.tolist(), int(cols[e])) - 1
+        return ((C - R) % p) * p + R
+    order = sorted(range(nnz), key=lambda e: (slot(e), int(rows[e]), e))
+    counts = np.bincount([slot(e) for e in range(nnz)], minlength=p * p)
+    bp, perm = oracle.bucket_cuts(n, m, p, rc, cc, rows, cols)
+    assert perm.tolist() == order
+    assert bp.tolist() == np.r_[0, np.cumsum(counts)].tolist()
+
+
 def test_bucket_invariants_medium_shape():
     w = make_config("medium", nnz=300_000, n=7_000, m=1_000, p=32)
     n, m, p = w.n, w.m, w.p
