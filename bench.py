@@ -45,6 +45,10 @@ def parse():
     ap.add_argument("--balanced-cuts", type=int, default=0, metavar="MAX_COLS",
                     help="use nnz-balanced block boundaries (at most MAX_COLS columns per "
                          "column-block) instead of the paper's equal blocks; 0 = equal blocks")
+    ap.add_argument("--single-column", type=int, default=1, choices=(0, 1),
+                    help="BGMF_OPT_SINGLE_COLUMN: 1 (default) lets blocks of a one-column "
+                         "column-block keep v in registers, 0 sends them through the "
+                         "general step")
     ap.add_argument("--variant-steps", type=int, default=3,
                     help="after the timed region, also time this many epochs with nnz-balanced "
                          "blocks (reported as a separate object; 0 disables)")
@@ -194,6 +198,7 @@ def main():
     mdl.set_option(bgmf.BGMF_OPT_XCD_REMAP, args.xcd_remap)
     mdl.set_option(bgmf.BGMF_OPT_V_STAGING, args.v_staging)
     mdl.set_option(bgmf.BGMF_OPT_BLOCK_PASSES, args.passes)
+    mdl.set_option(bgmf.BGMF_OPT_SINGLE_COLUMN, args.single_column)
     if args.balanced_cuts > 0:
         rc, cc = bgmf.bgmf_balanced_cuts(w.n, w.m, w.p, w.rows, w.cols, 65536, args.balanced_cuts)
         mdl.set_cuts(rc, cc)
@@ -264,6 +269,7 @@ def main():
         with bgmf.Model(w.n, w.m, w.k, w.p) as vm:
             vm.set_stream(stream.cuda_stream)
             vm.set_cuts(rc, cc)
+            vm.set_option(bgmf.BGMF_OPT_SINGLE_COLUMN, args.single_column)
             vm.set_factors(w.U0, w.V0)
             vm.load_coo(w.rows, w.cols, w.vals)
             vchain = [int(x) for x in vm.chain_stats()]

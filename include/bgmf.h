@@ -240,6 +240,15 @@ int bgmf_factor_ptrs(bgmf_t *h, float **U_dev, float **V_dev);
                                     Takes effect at the next bgmf_epoch, so a caller
                                     can vary it from epoch to epoch (the paper's
                                     variable block iterations). */
+#define BGMF_OPT_SINGLE_COLUMN 11 /* 1 (default): with V staged in LDS, a block
+                                    whose column-block is one column wide (a heavy
+                                    item given a column-block of its own through
+                                    bgmf_set_cuts) keeps that column's v in
+                                    registers from its first rating to its last,
+                                    instead of a write and a read of LDS per
+                                    rating; 0: such blocks take the general step.
+                                    The arithmetic is the same, so the results are
+                                    bit-identical. */
 int bgmf_set_option(bgmf_t *h, int32_t option, int64_t value);
 int bgmf_get_option(const bgmf_t *h, int32_t option, int64_t *value);
 

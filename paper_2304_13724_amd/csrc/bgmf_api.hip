@@ -48,6 +48,7 @@ struct bgmf {
   bool coop_lds = false, coop_gv = false;
   // options
   int64_t schedule = 0, wait_us = 10000000, xcd_remap = 1, v_staging = 0, passes = 1;
+  int64_t single_col = 1;
   // timing
   hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
   bool epoch_timed = false, rmse_timed = false;
@@ -629,6 +630,7 @@ int bgmf_epoch(bgmf_t *h, float alpha, float beta) {
   P.beta = beta;
   P.xcd_remap = (int32_t)h->xcd_remap;
   P.passes = (int32_t)h->passes;
+  P.single_col = (int32_t)h->single_col;
   const SweepShape sh = sweep_shape(h);
   HIP_TRY(h, hipEventRecord(h->ev[0], h->stream));
   if (h->ooc) {
@@ -970,6 +972,10 @@ int bgmf_set_option(bgmf_t *h, int32_t option, int64_t value) {
       if (value < 1 || value > 1024) return fail(h, BGMF_E_ARG, "block passes must be in [1, 1024]");
       h->passes = value;
       return BGMF_OK;
+    case BGMF_OPT_SINGLE_COLUMN:
+      if (value != 0 && value != 1) return fail(h, BGMF_E_ARG, "single column must be 0 or 1");
+      h->single_col = value;
+      return BGMF_OK;
     case BGMF_OPT_STREAM_CHUNKS:
       return fail(h, BGMF_E_ARG, "BGMF_OPT_STREAM_CHUNKS is read-only");
     case BGMF_OPT_RESIDENT_STRATA:
@@ -993,6 +999,7 @@ int bgmf_get_option(const bgmf_t *h, int32_t option, int64_t *value) {
       return BGMF_OK;
     case BGMF_OPT_RESIDENT_STRATA: *value = h->ooc ? h->s_res : h->p; return BGMF_OK;
     case BGMF_OPT_BLOCK_PASSES: *value = h->passes; return BGMF_OK;
+    case BGMF_OPT_SINGLE_COLUMN: *value = h->single_col; return BGMF_OK;
     case BGMF_OPT_PLACEMENT: {
       const SweepShape sh = sweep_shape(h);
       *value = (sh.lds ? 1 : 2) | (sh.persistent ? 4 : 0);

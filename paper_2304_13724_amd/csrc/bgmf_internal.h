@@ -73,6 +73,7 @@ struct SgdParams {
   float alpha, beta;
   int32_t xcd_remap;
   int32_t passes;            // sweeps of each block before the next (GPU_STEPS >= 1)
+  int32_t single_col;        // 1: blocks of a one-column column-block keep v in registers
 };
 constexpr int kFlagStride = 16;  // int64 words per flag (one 128-byte line)
 constexpr int kWavesPerGroup = 4;

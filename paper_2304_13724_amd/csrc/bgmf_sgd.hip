@@ -343,8 +343,17 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
       // step is a real rating and U is addressed with the row as a scalar
       // offset; the last, partial chunk of a block sends the U store of each
       // step past the end to an out-of-range vector offset (dropped).
-      auto chunk = [&](auto tail_tag, int32_t c) {
+      //
+      // ONE: the column-block is one column wide (a heavy item on its own,
+      // with cut points of unequal blocks), so every rating of the block
+      // updates the same v.  It then stays in registers for the whole block
+      // and goes back to its LDS slot once at the end, instead of a write
+      // and a read of LDS per rating; the arithmetic of every step is the
+      // same, so are the results.  The choice is made per block, so the
+      // prefetch ring keeps one register assignment inside each loop.
+      auto chunk = [&](auto tail_tag, auto one_tag, int32_t c) {
         constexpr bool TAIL = decltype(tail_tag)::value;
+        constexpr bool ONE = decltype(one_tag)::value;
         // records c .. c+63 are decoded and those of chunk c+CH are in
         // flight; fetch the window two chunks ahead now
         const uint2 Wn2 = rp[c + 2 * CH + lane];
@@ -365,7 +374,7 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
           // value computed below is forwarded instead
           const uint32_t raddr = vbase + col1;
           float vl[NV];
-          lds_ld<NV>(vl, ldsb, raddr);
+          if constexpr (!ONE) lds_ld<NV>(vl, ldsb, raddr);
 
           float tpart = fmaf(-u[0], vv[0], x64);
 #pragma unroll
@@ -377,7 +386,7 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
             nu[v] = u[v] + fmaf(ae, vv[v], nab * u[v]);
             nv[v] = vv[v] + fmaf(ae, u[v], nab * vv[v]);
           }
-          lds_st<NV>(nv, ldsb, waddr);
+          if constexpr (!ONE) lds_st<NV>(nv, ldsb, waddr);
           if constexpr (TAIL)
             st_row<NV, 0>(nu, Ures, doff + ((c + j < len) ? row : kOff), 0);
           else
@@ -385,11 +394,18 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
 #pragma unroll
           for (int v = 0; v < NV; ++v) {
             uprev[v] = nu[v];
-            vnext[v] = (col1 == ccur) ? nv[v] : vl[v];
+            if constexpr (!ONE)
+              vnext[v] = (col1 == ccur) ? nv[v] : vl[v];
+            else if constexpr (TAIL)
+              vnext[v] = (c + j < len) ? nv[v] : vv[v];  // steps past the end change nothing
+            else
+              vnext[v] = nv[v];
           }
           prev_row = row;
-          ccur = col1;
-          waddr = raddr;
+          if constexpr (!ONE) {
+            ccur = col1;
+            waddr = raddr;
+          }
           // prefetch the u row of rating t + D into the slot just freed
           ringrow[j] = rl(wrow, j + D);
           ld_row<NV, 0>(ring[j], Ures, doff, ringrow[j]);
@@ -397,9 +413,16 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
         decode(Wn1, c + CH);
         Wn1 = Wn2;
       };
+
       const int32_t full = len & ~(CH - 1);
-      for (int32_t c = 0; c < full; c += CH) chunk(std::false_type{}, c);
-      if (full < len) chunk(std::true_type{}, full);
+      if (ncols == 1 && P.single_col) {
+        for (int32_t c = 0; c < full; c += CH) chunk(std::false_type{}, std::true_type{}, c);
+        if (full < len) chunk(std::true_type{}, std::true_type{}, full);
+        lds_st<NV>(vnext, ldsb, waddr);
+      } else {
+        for (int32_t c = 0; c < full; c += CH) chunk(std::false_type{}, std::false_type{}, c);
+        if (full < len) chunk(std::true_type{}, std::false_type{}, full);
+      }
       }
       // publish the column slice, 16 columns per round (stores past the
       // slice are dropped)

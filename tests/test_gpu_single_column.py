@@ -1,0 +1,148 @@
+"""Blocks of a one-column column-block (BGMF_OPT_SINGLE_COLUMN): the sweep
+that keeps that column's v in registers through the block gives the same bits
+as the general step, and matches the oracle's epoch (Algorithm 1, Eq. 2-3)
+on the same layout.
+
+The crafted workload puts one heavy column alone in each of the first three
+column-blocks (every user rates it) and plants what the register path must
+still get right: a duplicate rating whose two copies straddle a chunk
+boundary (the first rating of a chunk repeats the row before it, so u is
+forwarded), a duplicate inside a chunk, blocks whose length is not a multiple
+of the chunk, and a column-block with many columns beside them.
+"""
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from helpers import row_rel_err
+from workloads import init_factors, make_config
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-4
+THREADS = min(16, os.cpu_count() or 1)
+
+
+class _W:
+    pass
+
+
+def _crafted(k, seed=7):
+    """n users, heavy columns 0, 1, 2 in column-blocks of their own, the other
+    columns in the last block; duplicates of rows 15 (copies at block
+    positions 15 and 16) and 40 in every heavy column, and of row 520 of
+    column 1 (second row-block)."""
+    n, m, p = 2_000, 61, 4
+    rng = np.random.default_rng(seed)
+    rows, cols = [], []
+    for j in (0, 1, 2):
+        r = np.arange(n)
+        r = np.sort(np.r_[r, 15, 40, 520 if j == 1 else 41])
+        rows.append(r)
+        cols.append(np.full(len(r), j))
+    extra = 30_000
+    rows.append(rng.integers(0, n, extra))
+    cols.append(rng.integers(3, m, extra))
+    rows = np.concatenate(rows).astype(np.int32)
+    cols = np.concatenate(cols).astype(np.int32)
+    order = rng.permutation(len(rows))  # input order does not matter to the layout
+    w = _W()
+    w.n, w.m, w.k, w.p = n, m, k, p
+    w.rows, w.cols = rows[order], cols[order]
+    w.vals = rng.integers(1, 6, len(rows)).astype(np.float32)
+    w.U0, w.V0 = init_factors(n, m, k, seed)
+    w.alpha, w.beta = 0.01, 0.05
+    rc = np.array([(R * n + p - 1) // p for R in range(p + 1)], dtype=np.int64)
+    cc = np.array([0, 1, 2, 3, m], dtype=np.int64)
+    return w, rc, cc
+
+
+def _gpu(w, rc, cc, single, epochs=2, schedule=0, passes=1):
+    from paper_2304_13724_amd import bgmf
+    with bgmf.Model(w.n, w.m, w.k, w.p) as mdl:
+        mdl.set_cuts(rc, cc)
+        mdl.set_option(bgmf.BGMF_OPT_V_STAGING, 1)
+        mdl.set_option(bgmf.BGMF_OPT_SCHEDULE, schedule)
+        mdl.set_option(bgmf.BGMF_OPT_BLOCK_PASSES, passes)
+        mdl.set_option(bgmf.BGMF_OPT_SINGLE_COLUMN, single)
+        assert mdl.get_option(bgmf.BGMF_OPT_SINGLE_COLUMN) == single
+        mdl.set_factors(w.U0, w.V0)
+        mdl.load_coo(w.rows, w.cols, w.vals)
+        hist = []
+        for _ in range(epochs):
+            mdl.epoch(w.alpha, w.beta)
+            hist.append(mdl.rmse())
+        U, V = mdl.get_factors()
+    return U, V, hist
+
+
+def _oracle(w, rc, cc, epochs=2, passes=1):
+    bp, perm = oracle.bucket_cuts(w.n, w.m, w.p, rc, cc, w.rows, w.cols)
+    U, V = w.U0.copy(), w.V0.copy()
+    hist = []
+    for _ in range(epochs):
+        if passes == 1:
+            oracle.epoch_mt(w.p, w.rows, w.cols, w.vals, bp, perm, U, V, w.alpha, w.beta,
+                            THREADS)
+        else:
+            oracle.epoch_passes(w.p, w.rows, w.cols, w.vals, bp, perm, U, V, w.alpha, w.beta,
+                                passes)
+        hist.append(oracle.rmse(w.rows, w.cols, w.vals, U, V))
+    return U, V, hist
+
+
+def test_crafted_layout_has_the_planted_cases():
+    w, rc, cc = _crafted(64)
+    bp, perm = oracle.bucket_cuts(w.n, w.m, w.p, rc, cc, w.rows, w.cols)
+    p = w.p
+    # block (R = 0, C = 0) is stratum 0, slot 0: positions 15 and 16 hold row 15
+    blk = perm[bp[0]:bp[1]]
+    assert np.all(w.cols[blk] == 0)
+    assert w.rows[blk][15] == 15 and w.rows[blk][16] == 15
+    # block (R = 1, C = 1) is stratum 0, slot 1: holds the duplicate of row 520
+    blk = perm[bp[1]:bp[2]]
+    r = w.rows[blk]
+    assert np.all(w.cols[blk] == 1) and np.count_nonzero(r == 520) == 2
+    assert bp[p * p] == len(w.rows)
+    # one-column blocks whose length is not a multiple of 16
+    sizes = np.diff(bp).reshape(p, p)  # [s, R]; column-block (R + s) mod p
+    one = [sizes[s, R] for s in range(p) for R in range(p) if (R + s) % p < 3]
+    assert any(x % 16 for x in one)
+
+
+@pytest.mark.parametrize("k", [16, 48, 64, 128])
+@pytest.mark.parametrize("schedule", [0, 1])
+def test_crafted_same_bits_and_oracle(k, schedule):
+    w, rc, cc = _crafted(k)
+    on = _gpu(w, rc, cc, 1, schedule=schedule)
+    off = _gpu(w, rc, cc, 0, schedule=schedule)
+    assert np.array_equal(on[0], off[0]) and np.array_equal(on[1], off[1])
+    assert on[2] == off[2]
+    o = _oracle(w, rc, cc)
+    assert row_rel_err(on[0], o[0]) <= TOL and row_rel_err(on[1], o[1]) <= TOL
+    for a, b in zip(on[2], o[2]):
+        assert abs(a - b) <= TOL * b
+
+
+def test_crafted_passes():
+    w, rc, cc = _crafted(64)
+    on = _gpu(w, rc, cc, 1, epochs=1, passes=3)
+    off = _gpu(w, rc, cc, 0, epochs=1, passes=3)
+    assert np.array_equal(on[0], off[0]) and np.array_equal(on[1], off[1])
+    o = _oracle(w, rc, cc, epochs=1, passes=3)
+    assert row_rel_err(on[0], o[0]) <= TOL and row_rel_err(on[1], o[1]) <= TOL
+
+
+def test_balanced_heavy_items_same_bits():
+    """Zipf items with nnz-balanced cut points (heavy items isolated); the
+    register path is taken (the general step is slower on one column)."""
+    from paper_2304_13724_amd import bgmf
+    w = make_config("large", n=48_000, m=1_800, nnz=1_000_000, p=128)
+    rc, cc = bgmf.bgmf_balanced_cuts(w.n, w.m, w.p, w.rows, w.cols, 65536, 64)
+    assert int(np.diff(cc).min()) == 1  # some column-blocks hold one item
+    on = _gpu(w, rc, cc, 1)
+    off = _gpu(w, rc, cc, 0)
+    assert np.array_equal(on[0], off[0]) and np.array_equal(on[1], off[1])
+    assert on[2] == off[2]
