@@ -49,6 +49,13 @@ def parse():
                     help="BGMF_OPT_SINGLE_COLUMN: 1 (default) lets blocks of a one-column "
                          "column-block keep v in registers, 0 sends them through the "
                          "general step")
+    ap.add_argument("--model", type=int, default=1, choices=(0, 1),
+                    help="after the timed region, time one dependent chain of general steps "
+                         "(t_dep, for the chain bound N / (sum of stratum maxima x t_dep)) "
+                         "and a 1 GiB device copy")
+    ap.add_argument("--pmc-l2", default=None, metavar="CSV",
+                    help="summarise a rocprofv3 --pmc TCC_HIT_sum TCC_MISS_sum counter CSV "
+                         "(per-kernel L2 hit rate) and exit")
     ap.add_argument("--variant-steps", type=int, default=3,
                     help="after the timed region, also time this many epochs with nnz-balanced "
                          "blocks (reported as a separate object; 0 disables)")
@@ -117,16 +124,37 @@ def pmc_summary(fetch_csv, write_csv, calib_mib):
     return out
 
 
-def cpu_baseline(w, budget_s):
-    """Time the CPU oracle (its multithreaded blocked epoch) on the first
-    strata of the same workload, about budget_s seconds of work."""
+def pmc_l2(csv_path):
+    """Per-kernel L2 (TCC) hits, misses and hit rate from one rocprofv3
+    --pmc TCC_HIT_sum TCC_MISS_sum run (mean per dispatch)."""
+    import csv
+    import statistics
+
+    per = {}
+    for r in csv.DictReader(open(csv_path)):
+        per.setdefault(r["Kernel_Name"], {}).setdefault(r["Counter_Name"], []).append(
+            float(r["Counter_Value"]))
+    out = {}
+    for name, c in sorted(per.items()):
+        if "bgmfk" not in name or "TCC_HIT_sum" not in c or "TCC_MISS_sum" not in c:
+            continue
+        hit, miss = statistics.mean(c["TCC_HIT_sum"]), statistics.mean(c["TCC_MISS_sum"])
+        out[name] = {"dispatches": len(c["TCC_HIT_sum"]), "hits": hit, "misses": miss,
+                     "hit_rate": hit / (hit + miss) if hit + miss else None}
+    return out
+
+
+def cpu_baseline(w, budget_s, threads=None, layout=None):
+    """Time the CPU oracle (its blocked epoch, multithreaded or on one
+    thread) on the first strata of the same workload, about budget_s seconds
+    of work.  Returns (result, layout)."""
     import numpy as np
 
     import oracle
 
-    threads = min(16, os.cpu_count() or 1)
+    threads = threads or min(16, os.cpu_count() or 1)
     t0 = time.perf_counter()
-    bp, perm = oracle.bucket(w.n, w.m, w.p, w.rows, w.cols)
+    bp, perm = layout if layout is not None else oracle.bucket(w.n, w.m, w.p, w.rows, w.cols)
     t_bucket = time.perf_counter() - t0
     p = w.p
     U, V = w.U0.copy(), w.V0.copy()
@@ -161,11 +189,58 @@ def cpu_baseline(w, budget_s):
                    f"blocks, strata in order from stratum 0) on the same workload: {cnt} rating "
                    f"updates in {dt:.2f} s; oracle bucketing of all {w.nnz} ratings took "
                    f"{t_bucket:.1f} s (untimed)"),
-    }
+        "updates": cnt,
+        "seconds": dt,
+    }, (bp, perm)
+
+
+def chain_model(stream):
+    """Per-update time of one dependent chain on the general step (t_dep):
+    480,000 ratings of one column in a one-column column-block, p = 8, with
+    the register path switched off, so that every rating is a general step on
+    the ratings before it; and the bandwidth of a plain 1 GiB device copy."""
+    import numpy as np
+    import torch
+
+    from paper_2304_13724_amd import bgmf
+    from workloads import init_factors
+
+    n, m, k, p = 480_000, 8, 64, 8
+    rows = np.arange(n, dtype=np.int32)
+    cols = np.zeros(n, dtype=np.int32)
+    vals = np.random.default_rng(1).integers(1, 6, n).astype(np.float32)
+    U0, V0 = init_factors(n, m, k, 3)
+    with bgmf.Model(n, m, k, p) as mdl:
+        mdl.set_stream(stream.cuda_stream)
+        mdl.set_cuts(np.array([(r * n + p - 1) // p for r in range(p + 1)], dtype=np.int64),
+                     np.r_[np.arange(p), m].astype(np.int64))
+        mdl.set_option(bgmf.BGMF_OPT_SINGLE_COLUMN, 0)
+        mdl.set_factors(U0, V0)
+        mdl.load_coo(rows, cols, vals)
+        ts = []
+        for _ in range(4):
+            mdl.epoch(0.001, 0.05)
+            ts.append(mdl.timing()[0])
+    t_dep = min(ts[1:]) * 1e6 / n
+    src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(5):
+        dst.copy_(src)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    copy_gbs = 5 * 2 * src.numel() * 4 / (e0.elapsed_time(e1) / 1e3) / 1e9
+    del src, dst
+    return t_dep, copy_gbs
 
 
 def main():
     args = parse()
+    if args.pmc_l2:
+        print(json.dumps(pmc_l2(args.pmc_l2), indent=1))
+        return
     if args.pmc_summary:
         summ = pmc_summary(args.pmc_summary[0], args.pmc_summary[1], args.calib_copy_mib or 1024)
         sweep = [v for k, v in summ["kernels"].items() if "k_sgd_lds" in k]
@@ -290,7 +365,17 @@ def main():
             "max_col_block": vchain[0], "max_row_block": vchain[1],
         }
         log(f"balanced blocks: sweep {v_sweep:.2f} ms, step {v_step:.2f} ms")
-    cpu = cpu_baseline(w, args.cpu_seconds) if args.cpu_seconds > 0 else None
+    t_dep, copy_gbs = chain_model(stream) if args.model else (None, None)
+    cpu = None
+    if args.cpu_seconds > 0:
+        cpu, layout = cpu_baseline(w, args.cpu_seconds)
+        one, _ = cpu_baseline(w, args.cpu_seconds / 2, threads=1, layout=layout)
+        cpu["value_1_thread"] = one["value"]
+        cpu["sample"] += (f"; on one thread (the paper's CMF analogue): {one['updates']} "
+                          f"updates in {one['seconds']:.2f} s")
+        for d in (cpu, one):
+            d.pop("updates")
+            d.pop("seconds")
     out = {
         "metric": METRIC,
         "value": value,
@@ -331,7 +416,12 @@ def main():
         "load_bucket_s": t_load,
         "chain": {"max_col_block": chain[0], "max_row_block": chain[1],
                   "sum_stratum_max": chain[2], "nonempty_blocks": chain[3],
-                  "ns_per_update_on_col_chain": sweep_avg * 1e6 / max(chain[0], 1)},
+                  "ns_per_update_on_col_chain": sweep_avg * 1e6 / max(chain[0], 1),
+                  "t_dep_ns": t_dep,
+                  "bound_updates_per_s": (upd / (chain[2] * t_dep * 1e-9 * args.passes)
+                                          if t_dep else None)},
+        "hbm_copy_GBs": copy_gbs,
+        "frac_vs_copy": achieved / copy_gbs if copy_gbs else None,
         "rmse_last": rmses[-1],
         "wall_s": wall,
     }
