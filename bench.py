@@ -250,8 +250,8 @@ def main():
         print(json.dumps(res, indent=1))
         return
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1 "
-                          "(multi-GPU sharding is a design note, not built)"}))
+        print(json.dumps({"error": "the sweep runs on one GPU; --gpus must be 1 "
+                          "(sharding across GPUs is designed but not implemented)"}))
         sys.exit(2)
     import numpy as np
     import torch
