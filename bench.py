@@ -89,7 +89,8 @@ def _sha1(path):
 def pmc_summary(fetch_csv, write_csv, calib_mib):
     """Per-kernel HBM bytes from FETCH_SIZE / WRITE_SIZE (KiB per dispatch),
     each scaled by what the counter reads for the calibration copy (the
-    first copy dispatch after the fill of the calibration buffer)."""
+    first copy dispatch after the fill of the calibration buffer, torch's
+    FillFunctor kernel)."""
     import csv
     import statistics
 
@@ -111,6 +112,9 @@ def pmc_summary(fetch_csv, write_csv, calib_mib):
     true_kib = calib_mib * 1024.0
     cf, fetch = load(fetch_csv)
     cw, write = load(write_csv)
+    if not cf or not cw:
+        raise ValueError("no calibration copy (a copy after the fill of the calibration buffer) "
+                         "in the counter files; run the profiled bench with --calib-copy-mib")
     f_fetch, f_write = true_kib / cf, true_kib / cw
     out = {"calibration_copy_mib": calib_mib, "fetch_counter_kib": cf, "write_counter_kib": cw,
            "fetch_scale": f_fetch, "write_scale": f_write, "kernels": {}}
