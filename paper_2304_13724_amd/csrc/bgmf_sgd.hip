@@ -223,6 +223,8 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
   constexpr int KPL = L::KPL;
   constexpr int D = kPrefetch;
   constexpr int CH = D;  // ratings per unrolled chunk; ring slot = step in chunk
+  static_assert((CH & (CH - 1)) == 0 && CH <= 32,
+                "full chunks are counted with a mask; lanes j + D stay in the 64-record window");
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
   const int b = row_block_of_wave(P, wave);
   if (b >= P.p) return;
