@@ -86,6 +86,17 @@ def _sha1(path):
     return hashlib.sha1(open(path, "rb").read()).hexdigest()
 
 
+# how each synthetic workload is drawn (workloads/synth.py)
+STRUCTURE = {
+    "tiny": "distinct cells uniform at random, planted rank 8, values 1..5",
+    "medium": "power-law user degree, Zipf(1.1) items, planted rank 16, values 1..5",
+    "large": "lognormal user degree, Zipf(1.2) items",
+    "vlarge": "Zipf(1.1) users and items, continuous values in [0, 100]",
+    "ooc": "Zipf(1.1) users and items, planted rank 32, values 1..5",
+    "table1": "dense 1024 x 1024, integer values 1..30",
+}
+
+
 def pmc_summary(fetch_csv, write_csv, calib_mib):
     """Per-kernel HBM bytes from FETCH_SIZE / WRITE_SIZE (KiB per dispatch),
     each scaled by what the counter reads for the calibration copy (the
@@ -395,7 +406,7 @@ def main():
         "data": "synthetic",
         "config": {
             "workload": (f"{args.config}: n={w.n} users, m={w.m} items, {nnz} ratings "
-                         f"(lognormal user degree, Zipf(1.2) items), k={w.k}, p={w.p}, "
+                         f"({STRUCTURE.get(args.config, 'synthetic')}), k={w.k}, p={w.p}, "
                          f"alpha={w.alpha}, beta={w.beta}; step = one epoch + RMSE pass"
                          + (f"; {args.passes} passes per block" if args.passes > 1 else "")
                          + (f"; nnz-balanced blocks (at most {args.balanced_cuts} columns)"
