@@ -12,7 +12,8 @@
 // Per wave and block:
 //   * V: either the block's column slice (ncols x k fp32) is copied into LDS
 //     after the acquire, updated there and written back before the release
-//     (k_sgd_lds), or V stays in global memory and each rating's v row is
+//     (k_sgd_lds; a slice one column wide instead stays in registers for the
+//     whole block), or V stays in global memory and each rating's v row is
 //     prefetched like the u rows (k_sgd_gv, for slices too wide for LDS);
 //   * U rows are owned by the wave for the whole launch; they are prefetched
 //     from HBM kPrefetch ratings ahead into a register ring and stored after
@@ -24,7 +25,11 @@
 //     dimensions (one 4-, 8- or 16-byte access per row); the dot product is
 //     reduced across lanes with DPP row operations and row broadcasts.
 // There is no dense contraction here (each rating is a length-k dot product
-// on a serial dependency chain), so no MFMA is used.
+// on a serial dependency chain), so no MFMA is used.  (Regrouping a run of
+// ratings on one column into Gram matrices of U rows would make one; on
+// gfx950 each fp32 MFMA then costs more of the wave's issue time than it
+// saves, since this loop is issue-bound at about 5.5-6 cycles per
+// instruction.)
 #include <type_traits>
 
 #include "bgmf_internal.h"
