@@ -28,8 +28,14 @@
 // on a serial dependency chain), so no MFMA is used.  (Regrouping a run of
 // ratings on one column into Gram matrices of U rows would make one; on
 // gfx950 each fp32 MFMA then costs more of the wave's issue time than it
-// saves, since this loop is issue-bound at about 5.5-6 cycles per
-// instruction.)
+// saves.)
+//
+// Timing: a lone wave issues in order, one instruction per 4-cycle slot
+// (a lane read takes two, and every hazard wait state costs a slot).  Each
+// level of the cross-lane reduction must wait two states for the previous
+// one, so the LDS sweep places the step's independent instructions (stores,
+// lane reads, the ring refill, the next rating's v) in those gaps, and
+// scheduling fences keep them there.
 #include <type_traits>
 
 #include "bgmf_internal.h"
@@ -45,6 +51,10 @@ __device__ __forceinline__ float dpp_mov(float x) {
 __device__ __forceinline__ uint32_t rl(uint32_t v, int lane) {
   return (uint32_t)__builtin_amdgcn_readlane((int)v, lane);
 }
+
+// Scheduling fence: the compiler keeps the instructions on either side of
+// it in program order.
+__device__ __forceinline__ void pin() { __builtin_amdgcn_sched_barrier(0); }
 
 __device__ __forceinline__ int64_t uniform64(int64_t x) {
   const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)x);
@@ -334,22 +344,48 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
       // one address in order)
       for (int pass = 0; pass < P.passes; ++pass) {
       if (pass > 0) prime();
-      uint32_t waddr = vbase + rl(wcol, 0);  // LDS address of the current column
-      float vnext[NV];
-      lds_ld<NV>(vnext, ldsb, waddr);
-      uint32_t prev_row = 0xFFFFFFFFu;
-      float uprev[NV];
-#pragma unroll
-      for (int v = 0; v < NV; ++v) uprev[v] = 0.0f;
+      // operands of the first step: its column, v, x and u
+      uint32_t ccur = rl(wcol, 0);  // LDS byte offset of the current column
+      char *const vb = ldsb + vbase;  // this lane's part of the wave's LDS column slots
+      char *waddr = vb + ccur;
+      float u[NV], vv[NV];
+      lds_ld<NV>(vv, waddr, 0);
+      uint32_t x64 = rl(__float_as_uint(wx), 0);
+      uint32_t ncol = rl(wcol, 1);  // column of the next rating
+      char *naddr = vb + ncol;
       // The ring loads were issued before the wait and the V staging, so
       // they have landed; saying so explicitly (vmcnt(0)) lets the compiler
       // count outstanding loads inside the loop from its steady state alone.
       __builtin_amdgcn_s_waitcnt(0x0F70);
+#pragma unroll
+      for (int v = 0; v < NV; ++v) u[v] = ring[0][v];
+      // Results of a step are stored during the next step's reduction; at
+      // the start the pending results are rating 0's current u and v,
+      // written back unchanged.
+      float pnu[NV], pnv[NV];
+      uint32_t prow = ringrow[0];
+      char *pwaddr = waddr;
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        pnu[v] = u[v];
+        pnv[v] = vv[v];
+      }
 
       // One chunk of CH ratings, fully unrolled.  In a full chunk every
       // step is a real rating and U is addressed with the row as a scalar
       // offset; the last, partial chunk of a block sends the U store of each
       // step past the end to an out-of-range vector offset (dropped).
+      //
+      // A step is one dependent chain: partial products, six cross-lane
+      // levels, the lane read of e, the update, and the choice of the next
+      // step's operands.  A lone wave issues in order, so every other
+      // instruction of the step (the stores of the previous step's u and
+      // v, the next rating's v, the lane reads of later rows, columns and x,
+      // the ring refill, the row and column compares, the decay products)
+      // is placed between the reduction levels, where the chain leaves
+      // issue slots free anyway (each level waits two states for the
+      // previous one); the fences keep that order.  The arithmetic is that
+      // of the plain order, so the results are the same bits.
       //
       // ONE: the column-block is one column wide (a heavy item on its own,
       // with cut points of unequal blocks), so every rating of the block
@@ -364,71 +400,109 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
         // records c .. c+63 are decoded and those of chunk c+CH are in
         // flight; fetch the window two chunks ahead now
         const uint2 Wn2 = rp[c + 2 * CH + lane];
-        uint32_t ccur = rl(wcol, 0);
 #pragma unroll
         for (int j = 0; j < CH; ++j) {
-          const float x64 = __uint_as_float(rl(__float_as_uint(wx), j));
-          const uint32_t row = ringrow[j];
-          const uint32_t col1 = rl(wcol, j + 1);
-          const bool same_row = row == prev_row;
-          float u[NV], vv[NV];
+          const int slot = (j == 0) ? CH - 1 : j - 1;  // ring slot of the previous rating
+          const int next = (j + 1) % CH;               // ring slot of the next rating
+          float t = fmaf(-u[0], vv[0], __uint_as_float(x64));
 #pragma unroll
-          for (int v = 0; v < NV; ++v) {
-            u[v] = same_row ? uprev[v] : ring[j][v];
-            vv[v] = vnext[v];
-          }
-          // read v of the next rating now; if it is the same column the
-          // value computed below is forwarded instead
-          const uint32_t raddr = vbase + col1;
+          for (int v = 1; v < NV; ++v) t = fmaf(-u[v], vv[v], t);
+          pin();
+          // the previous step's v, then the next rating's v (after that
+          // store; if it is this step's column, the new value is forwarded
+          // instead)
           float vl[NV];
-          if constexpr (!ONE) lds_ld<NV>(vl, ldsb, raddr);
-
-          float tpart = fmaf(-u[0], vv[0], x64);
+          if constexpr (!ONE) {
+            lds_st<NV>(pnv, pwaddr, 0);
+            lds_ld<NV>(vl, naddr, 0);
+          }
+          pin();
+          t = t + dpp_mov<0xB1>(t);  // quad_perm [1,0,3,2]
+          pin();
+          // the previous step's u; the row of the rating D after the
+          // previous one, whose ring slot is free again (its value was
+          // consumed one step ago)
+          if constexpr (TAIL)
+            st_row<NV, 0>(pnu, Ures, doff + ((c + j - 1 < len) ? prow : kOff), 0);
+          else
+            st_row<NV, 0>(pnu, Ures, doff, prow);
+          ringrow[slot] = rl(wrow, slot + D - (j == 0 ? CH : 0));
+          pin();
+          t = t + dpp_mov<0x4E>(t);  // quad_perm [2,3,0,1]
+          pin();
+          const uint32_t col2 = rl(wcol, j + 2);  // the column after the next one
+          float du[NV], dv[NV];
 #pragma unroll
-          for (int v = 1; v < NV; ++v) tpart = fmaf(-u[v], vv[v], tpart);
-          const float ae = alpha * lane_total<KPL>(tpart);
+          for (int v = 0; v < NV; ++v) du[v] = nab * u[v];
+          pin();
+          t = t + dpp_mov<0x141>(t);  // row_half_mirror
+          pin();
+#pragma unroll
+          for (int v = 0; v < NV; ++v) dv[v] = nab * vv[v];
+          ld_row<NV, 0>(ring[slot], Ures, doff, ringrow[slot]);
+          pin();
+          t = t + dpp_mov<0x140>(t);  // row_mirror
+          pin();
+          const bool same_row = ringrow[next] == ringrow[j];
+          pin();
+          if constexpr (KPL >= 32) t = t + dpp_mov<0x142>(t);  // row_bcast:15
+          pin();
+          if constexpr (KPL >= 64) t = t + dpp_mov<0x143>(t);  // row_bcast:31
+          pin();
+          const bool same_col = ncol == ccur;
+          pin();
+          const float e = __uint_as_float(rl(__float_as_uint(t), 63));
+          pin();
+          const uint32_t x64n = rl(__float_as_uint(wx), j + 1);
+          pin();
+          const float ae = alpha * e;
           float nu[NV], nv[NV];
 #pragma unroll
           for (int v = 0; v < NV; ++v) {
-            nu[v] = u[v] + fmaf(ae, vv[v], nab * u[v]);
-            nv[v] = vv[v] + fmaf(ae, u[v], nab * vv[v]);
+            nu[v] = u[v] + fmaf(ae, vv[v], du[v]);
+            nv[v] = vv[v] + fmaf(ae, u[v], dv[v]);
           }
-          if constexpr (!ONE) lds_st<NV>(nv, ldsb, waddr);
-          if constexpr (TAIL)
-            st_row<NV, 0>(nu, Ures, doff + ((c + j < len) ? row : kOff), 0);
-          else
-            st_row<NV, 0>(nu, Ures, doff, row);
+          prow = ringrow[j];
+          pwaddr = waddr;
 #pragma unroll
           for (int v = 0; v < NV; ++v) {
-            uprev[v] = nu[v];
+            pnu[v] = nu[v];
+            pnv[v] = nv[v];
+            u[v] = same_row ? nu[v] : ring[next][v];
             if constexpr (!ONE)
-              vnext[v] = (col1 == ccur) ? nv[v] : vl[v];
+              vv[v] = same_col ? nv[v] : vl[v];
             else if constexpr (TAIL)
-              vnext[v] = (c + j < len) ? nv[v] : vv[v];  // steps past the end change nothing
+              vv[v] = (c + j < len) ? nv[v] : vv[v];  // steps past the end change nothing
             else
-              vnext[v] = nv[v];
+              vv[v] = nv[v];
           }
-          prev_row = row;
+          x64 = x64n;
           if constexpr (!ONE) {
-            ccur = col1;
-            waddr = raddr;
+            ccur = ncol;
+            waddr = naddr;
+            ncol = col2;
+            naddr = vb + col2;
           }
-          // prefetch the u row of rating t + D into the slot just freed
-          ringrow[j] = rl(wrow, j + D);
-          ld_row<NV, 0>(ring[j], Ures, doff, ringrow[j]);
+          pin();
         }
         decode(Wn1, c + CH);
         Wn1 = Wn2;
       };
 
+      // The results of the block's last step are still pending; after a
+      // partial chunk they belong to a step past the end (its u store is
+      // dropped, its v store lands in the spare slot).
       const int32_t full = len & ~(CH - 1);
       if (ncols == 1 && P.single_col) {
         for (int32_t c = 0; c < full; c += CH) chunk(std::false_type{}, std::true_type{}, c);
         if (full < len) chunk(std::true_type{}, std::true_type{}, full);
-        lds_st<NV>(vnext, ldsb, waddr);
+        if (full == len) st_row<NV, 0>(pnu, Ures, doff, prow);
+        lds_st<NV>(vv, waddr, 0);
       } else {
         for (int32_t c = 0; c < full; c += CH) chunk(std::false_type{}, std::false_type{}, c);
         if (full < len) chunk(std::true_type{}, std::false_type{}, full);
+        if (full == len) st_row<NV, 0>(pnu, Ures, doff, prow);
+        lds_st<NV>(pnv, pwaddr, 0);
       }
       }
       // publish the column slice, 16 columns per round (stores past the
