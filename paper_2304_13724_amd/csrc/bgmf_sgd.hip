@@ -126,6 +126,40 @@ struct LdsVec<2> { using T = float2; };
 template <>
 struct LdsVec<4> { using T = float4; };
 
+// LDS pointers: an address kept in a register across steps stays an LDS
+// address (ds_read / ds_write), which a generic pointer would not.
+using lds_char = __attribute__((address_space(3))) char;
+template <int NV>
+struct LdsRaw { using T = float __attribute__((ext_vector_type(NV))); };
+template <>
+struct LdsRaw<1> { using T = float; };
+
+// One lane's share of a row in LDS through an LDS pointer.
+template <int NV>
+__device__ __forceinline__ void lds_ld(float (&x)[NV], const lds_char *p) {
+  using T = typename LdsRaw<NV>::T;
+  const T t = *reinterpret_cast<const __attribute__((address_space(3))) T *>(p);
+  if constexpr (NV == 1) {
+    x[0] = t;
+  } else {
+#pragma unroll
+    for (int v = 0; v < NV; ++v) x[v] = t[v];
+  }
+}
+
+template <int NV>
+__device__ __forceinline__ void lds_st(const float (&x)[NV], lds_char *p) {
+  using T = typename LdsRaw<NV>::T;
+  T t;
+  if constexpr (NV == 1) {
+    t = x[0];
+  } else {
+#pragma unroll
+    for (int v = 0; v < NV; ++v) t[v] = x[v];
+  }
+  *reinterpret_cast<__attribute__((address_space(3))) T *>(p) = t;
+}
+
 template <int NV>
 __device__ __forceinline__ void lds_ld(float (&x)[NV], const char *base, uint32_t off) {
   const auto t = *reinterpret_cast<const typename LdsVec<NV>::T *>(base + off);
@@ -346,13 +380,13 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
       if (pass > 0) prime();
       // operands of the first step: its column, v, x and u
       uint32_t ccur = rl(wcol, 0);  // LDS byte offset of the current column
-      char *const vb = ldsb + vbase;  // this lane's part of the wave's LDS column slots
-      char *waddr = vb + ccur;
+      lds_char *const vb = (lds_char *)ldsb + vbase;  // this lane's part of the wave's LDS column slots
+      lds_char *waddr = vb + ccur;
       float u[NV], vv[NV];
-      lds_ld<NV>(vv, waddr, 0);
+      lds_ld<NV>(vv, waddr);
       uint32_t x64 = rl(__float_as_uint(wx), 0);
       uint32_t ncol = rl(wcol, 1);  // column of the next rating
-      char *naddr = vb + ncol;
+      lds_char *naddr = vb + ncol;
       // The ring loads were issued before the wait and the V staging, so
       // they have landed; saying so explicitly (vmcnt(0)) lets the compiler
       // count outstanding loads inside the loop from its steady state alone.
@@ -364,7 +398,7 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
       // written back unchanged.
       float pnu[NV], pnv[NV];
       uint32_t prow = ringrow[0];
-      char *pwaddr = waddr;
+      lds_char *pwaddr = waddr;
 #pragma unroll
       for (int v = 0; v < NV; ++v) {
         pnu[v] = u[v];
@@ -413,19 +447,21 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
           // instead)
           float vl[NV];
           if constexpr (!ONE) {
-            lds_st<NV>(pnv, pwaddr, 0);
-            lds_ld<NV>(vl, naddr, 0);
+            lds_st<NV>(pnv, pwaddr);
+            lds_ld<NV>(vl, naddr);
           }
           pin();
           t = t + dpp_mov<0xB1>(t);  // quad_perm [1,0,3,2]
           pin();
-          // the previous step's u; the row of the rating D after the
+          // the previous step's u, then the row of the rating D after the
           // previous one, whose ring slot is free again (its value was
-          // consumed one step ago)
+          // consumed one step ago); this order is measurably faster than
+          // the lane read first
           if constexpr (TAIL)
             st_row<NV, 0>(pnu, Ures, doff + ((c + j - 1 < len) ? prow : kOff), 0);
           else
             st_row<NV, 0>(pnu, Ures, doff, prow);
+          pin();
           ringrow[slot] = rl(wrow, slot + D - (j == 0 ? CH : 0));
           pin();
           t = t + dpp_mov<0x4E>(t);  // quad_perm [2,3,0,1]
@@ -439,6 +475,7 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
           pin();
 #pragma unroll
           for (int v = 0; v < NV; ++v) dv[v] = nab * vv[v];
+          pin();
           ld_row<NV, 0>(ring[slot], Ures, doff, ringrow[slot]);
           pin();
           t = t + dpp_mov<0x140>(t);  // row_mirror
@@ -447,13 +484,26 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
           pin();
           if constexpr (KPL >= 32) t = t + dpp_mov<0x142>(t);  // row_bcast:15
           pin();
+          const bool same_col = ncol == ccur;
+          pin();
           if constexpr (KPL >= 64) t = t + dpp_mov<0x143>(t);  // row_bcast:31
           pin();
-          const bool same_col = ncol == ccur;
+          // the next rating's x: before the lane read of e in the general
+          // step, after it in the one-column step
+          uint32_t x64n;
+          if constexpr (!ONE) x64n = rl(__float_as_uint(wx), j + 1);
           pin();
           const float e = __uint_as_float(rl(__float_as_uint(t), 63));
           pin();
-          const uint32_t x64n = rl(__float_as_uint(wx), j + 1);
+          if constexpr (ONE) x64n = rl(__float_as_uint(wx), j + 1);
+          // LDS address of the column after the next one, computed here;
+          // the empty asm keeps the compiler from recomputing it next to
+          // its use, where it would take a slot the gaps above need
+          lds_char *naddr2 = nullptr;
+          if constexpr (!ONE) {
+            naddr2 = vb + col2;
+            asm volatile("" : "+v"(naddr2));
+          }
           pin();
           const float ae = alpha * e;
           float nu[NV], nv[NV];
@@ -481,7 +531,7 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
             ccur = ncol;
             waddr = naddr;
             ncol = col2;
-            naddr = vb + col2;
+            naddr = naddr2;
           }
           pin();
         }
@@ -497,12 +547,12 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
         for (int32_t c = 0; c < full; c += CH) chunk(std::false_type{}, std::true_type{}, c);
         if (full < len) chunk(std::true_type{}, std::true_type{}, full);
         if (full == len) st_row<NV, 0>(pnu, Ures, doff, prow);
-        lds_st<NV>(vv, waddr, 0);
+        lds_st<NV>(vv, waddr);
       } else {
         for (int32_t c = 0; c < full; c += CH) chunk(std::false_type{}, std::false_type{}, c);
         if (full < len) chunk(std::true_type{}, std::false_type{}, full);
         if (full == len) st_row<NV, 0>(pnu, Ures, doff, prow);
-        lds_st<NV>(pnv, pwaddr, 0);
+        lds_st<NV>(pnv, pwaddr);
       }
       }
       // publish the column slice, 16 columns per round (stores past the
