@@ -28,6 +28,7 @@ struct bgmf {
   // ratings layout
   int64_t nnz = 0;
   int64_t *block_ptr = nullptr, *wblock_ptr = nullptr;
+  uint8_t *rowrep = nullptr;  // [p*p] per block slot: a row repeats in consecutive ratings
   int32_t *perm = nullptr;
   uint2 *rec = nullptr;
   int64_t *flags = nullptr;
@@ -99,6 +100,7 @@ void free_layout(bgmf_t *h) {
   if (h->side) hipStreamSynchronize(h->side);
   hipFree(h->block_ptr);
   hipFree(h->wblock_ptr);
+  hipFree(h->rowrep);
   hipFree(h->perm);
   hipFree(h->rec);
   hipFree(h->ring);
@@ -112,6 +114,7 @@ void free_layout(bgmf_t *h) {
   h->slot_used.clear();
   h->chunk.clear();
   h->block_ptr = h->wblock_ptr = nullptr;
+  h->rowrep = nullptr;
   h->perm = nullptr;
   h->rec = h->ring = h->host_rec = h->resident = nullptr;
   h->s_res = 0;
@@ -162,7 +165,7 @@ hipError_t configure_sweep(bgmf_t *h) {
   hipError_t e;
   for (int vm : {kVLds, kVGlobal, kVGlobalCoherent})
     if ((e = sgd_set_lds_limit(h->kp, mask, vm, h->lds_limit)) != hipSuccess) return e;
-  const size_t slice = (size_t)(h->cols_max + 1) * h->kp * sizeof(float);
+  const size_t slice = sgd_lds_per_wave(h->kp, h->cols_max);
   h->wpg_lds = kWavesPerGroup;
   while (h->wpg_lds > 1 && h->wpg_lds * slice > h->lds_limit) h->wpg_lds >>= 1;
   h->lds_bytes_lds = h->wpg_lds * slice;
@@ -385,6 +388,7 @@ int bgmf_load_coo(bgmf_t *h, const int32_t *rows, const int32_t *cols, const flo
   LOAD_TRY(hipMalloc(&scratch, scratch_bytes));
   LOAD_TRY(hipMalloc(&h->block_ptr, (size_t)(slots + 1) * sizeof(int64_t)));
   LOAD_TRY(hipMalloc(&h->wblock_ptr, (size_t)(slots + 1) * sizeof(int64_t)));
+  LOAD_TRY(hipMalloc(&h->rowrep, (size_t)slots));
   LOAD_TRY(hipMalloc(&h->perm, (size_t)nnz * sizeof(int32_t)));
   LOAD_TRY(hipMalloc(&h->rec, (size_t)(nnz + kRecPad) * sizeof(uint2)));
   LOAD_TRY(hipMemcpyAsync(d_rows, rows, (size_t)nnz * sizeof(int32_t), hipMemcpyHostToDevice,
@@ -393,8 +397,9 @@ int bgmf_load_coo(bgmf_t *h, const int32_t *rows, const int32_t *cols, const flo
                           h->stream));
   LOAD_TRY(hipMemcpyAsync(d_vals, vals, (size_t)nnz * sizeof(float), hipMemcpyHostToDevice,
                           h->stream));
-  BucketOut out{h->block_ptr, h->wblock_ptr, h->perm, h->rec};
+  BucketOut out{h->block_ptr, h->wblock_ptr, h->perm, h->rec, h->rowrep};
   LOAD_TRY(hipMemsetAsync(h->err, 0, sizeof(int32_t), h->stream));
+  LOAD_TRY(hipMemsetAsync(h->rowrep, 0, (size_t)slots, h->stream));
   // ratings that do not fit the budget are kept stratum-major, so that each
   // stratum is one contiguous range to stream
   const bool ooc = h->budget > 0 && (nnz + kRecPad) * (int64_t)sizeof(uint2) > h->budget;
@@ -631,6 +636,7 @@ int bgmf_epoch(bgmf_t *h, float alpha, float beta) {
   P.xcd_remap = (int32_t)h->xcd_remap;
   P.passes = (int32_t)h->passes;
   P.single_col = (int32_t)h->single_col;
+  P.rowrep = h->rowrep;
   const SweepShape sh = sweep_shape(h);
   HIP_TRY(h, hipEventRecord(h->ev[0], h->stream));
   if (h->ooc) {

@@ -250,7 +250,7 @@ __global__ void k_gather(const uint64_t *__restrict__ skeys, const int32_t *__re
                          const int32_t *__restrict__ cols, const float *__restrict__ vals,
                          int64_t nnz, Grid G, int rbits, const int64_t *__restrict__ block_ptr,
                          const int64_t *__restrict__ wblock_ptr, bool stratum_major,
-                         uint2 *__restrict__ rec, int32_t *err) {
+                         uint2 *__restrict__ rec, uint8_t *__restrict__ rowrep, int32_t *err) {
   const uint64_t rmask = (rbits == 0) ? 0ull : ((1ull << rbits) - 1ull);
   for (int64_t t = gid(); t < nnz; t += (int64_t)gridDim.x * blockDim.x) {
     const uint64_t key = skeys[t];
@@ -260,6 +260,9 @@ __global__ void k_gather(const uint64_t *__restrict__ skeys, const int32_t *__re
       continue;
     }
     const uint32_t lrow = (uint32_t)(key & rmask);
+    // equal sorted keys = same block and row: the block repeats a row in
+    // consecutive ratings (its rows ascend, so equal rows are adjacent)
+    if (t > 0 && skeys[t - 1] == key) rowrep[q] = 1;
     const int64_t s = q / G.p, b = q - s * G.p;
     const int64_t C = (b + s) % G.p;
     const int32_t e = perm[t];
@@ -365,7 +368,8 @@ hipError_t bucket(const int32_t *rows, const int32_t *cols, const float *vals, i
   hipLaunchKernelGGL(k_fill_rec, dim3(1), dim3(kThreads), 0, st, out.rec + nnz,
                      (int64_t)kRecPad);
   hipLaunchKernelGGL(k_gather, dim3(g), dim3(kThreads), 0, st, kin, vin, cols, vals, nnz, G,
-                     rbits, out.block_ptr, out.wblock_ptr, stratum_major, out.rec, err);
+                     rbits, out.block_ptr, out.wblock_ptr, stratum_major, out.rec, out.rowrep,
+                     err);
   return hipGetLastError();
 }
 

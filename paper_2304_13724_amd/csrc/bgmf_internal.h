@@ -74,6 +74,8 @@ struct SgdParams {
   int32_t xcd_remap;
   int32_t passes;            // sweeps of each block before the next (GPU_STEPS >= 1)
   int32_t single_col;        // 1: blocks of a one-column column-block keep v in registers
+  const uint8_t *rowrep;     // [p * p], slot s*p + b: 1 if two consecutive ratings of the
+                             // block share a row
 };
 constexpr int kFlagStride = 16;  // int64 words per flag (one 128-byte line)
 constexpr int kWavesPerGroup = 4;
@@ -95,6 +97,8 @@ hipError_t sgd_occupancy(int kp, bool mask, int vmode, int waves_per_group, size
                          int *groups_per_cu);
 hipError_t sgd_set_lds_limit(int kp, bool mask, int vmode, size_t lds_bytes);
 size_t sgd_gv_lds_per_wave(int kp);
+// LDS of one wave of the LDS sweep: cols_max + 1 column slots.
+size_t sgd_lds_per_wave(int kp, int cols_max);
 
 hipError_t launch_rmse(const uint2 *rec, const int64_t *wblock_ptr, const float *U,
                        const float *V, const Grid &G, int64_t rows_max, int32_t k, int64_t nnz,
@@ -126,6 +130,8 @@ struct BucketOut {
   int64_t *wblock_ptr;  // [p*p + 1] wave-major block starts
   int32_t *perm;        // [nnz] input position of each slot-ordered rating
   uint2 *rec;           // [nnz + kRecPad] wave-major records
+  uint8_t *rowrep;      // [p*p] slot q: 1 if two consecutive ratings of the block share a
+                        // row (set here; zeroed by the caller)
 };
 size_t bucket_scratch_bytes(int64_t nnz, int32_t p);
 // stratum_major: records in slot order (each stratum contiguous) instead of

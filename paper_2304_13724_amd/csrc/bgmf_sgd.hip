@@ -13,7 +13,8 @@
 //   * V: either the block's column slice (ncols x k fp32) is copied into LDS
 //     after the acquire, updated there and written back before the release
 //     (k_sgd_lds; a slice one column wide instead stays in registers for the
-//     whole block), or V stays in global memory and each rating's v row is
+//     whole block, with a shorter dependency chain per rating when no row
+//     repeats), or V stays in global memory and each rating's v row is
 //     prefetched like the u rows (k_sgd_gv, for slices too wide for LDS);
 //   * U rows are owned by the wave for the whole launch; they are prefetched
 //     from HBM kPrefetch ratings ahead into a register ring and stored after
@@ -320,6 +321,8 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
     const int64_t beg = uniform64(bx[0]);
     const int32_t len = (int32_t)(uniform64(bx[1]) - beg);
     const uint2 *rp = P.rec + (beg - P.rec_origin);
+    const bool fold = ncols == 1 && P.single_col &&
+                      __builtin_amdgcn_readfirstlane(P.rowrep[(int64_t)s * P.p + b]) == 0;
 
     // Decoded window of 64 records starting at chunk position c:
     //   wrow = byte offset of the row in U (row 0 past the block end, so the
@@ -420,17 +423,8 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
       // issue slots free anyway (each level waits two states for the
       // previous one); the fences keep that order.  The arithmetic is that
       // of the plain order, so the results are the same bits.
-      //
-      // ONE: the column-block is one column wide (a heavy item on its own,
-      // with cut points of unequal blocks), so every rating of the block
-      // updates the same v.  It then stays in registers for the whole block
-      // and goes back to its LDS slot once at the end, instead of a write
-      // and a read of LDS per rating; the arithmetic of every step is the
-      // same, so are the results.  The choice is made per block, so the
-      // prefetch ring keeps one register assignment inside each loop.
-      auto chunk = [&](auto tail_tag, auto one_tag, int32_t c) {
+      auto chunk = [&](auto tail_tag, int32_t c) {
         constexpr bool TAIL = decltype(tail_tag)::value;
-        constexpr bool ONE = decltype(one_tag)::value;
         // records c .. c+63 are decoded and those of chunk c+CH are in
         // flight; fetch the window two chunks ahead now
         const uint2 Wn2 = rp[c + 2 * CH + lane];
@@ -446,10 +440,8 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
           // store; if it is this step's column, the new value is forwarded
           // instead)
           float vl[NV];
-          if constexpr (!ONE) {
-            lds_st<NV>(pnv, pwaddr);
-            lds_ld<NV>(vl, naddr);
-          }
+          lds_st<NV>(pnv, pwaddr);
+          lds_ld<NV>(vl, naddr);
           pin();
           t = t + dpp_mov<0xB1>(t);  // quad_perm [1,0,3,2]
           pin();
@@ -488,22 +480,15 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
           pin();
           if constexpr (KPL >= 64) t = t + dpp_mov<0x143>(t);  // row_bcast:31
           pin();
-          // the next rating's x: before the lane read of e in the general
-          // step, after it in the one-column step
-          uint32_t x64n;
-          if constexpr (!ONE) x64n = rl(__float_as_uint(wx), j + 1);
+          const uint32_t x64n = rl(__float_as_uint(wx), j + 1);  // the next rating's x
           pin();
           const float e = __uint_as_float(rl(__float_as_uint(t), 63));
           pin();
-          if constexpr (ONE) x64n = rl(__float_as_uint(wx), j + 1);
           // LDS address of the column after the next one, computed here;
           // the empty asm keeps the compiler from recomputing it next to
           // its use, where it would take a slot the gaps above need
-          lds_char *naddr2 = nullptr;
-          if constexpr (!ONE) {
-            naddr2 = vb + col2;
-            asm volatile("" : "+v"(naddr2));
-          }
+          lds_char *naddr2 = vb + col2;
+          asm volatile("" : "+v"(naddr2));
           pin();
           const float ae = alpha * e;
           float nu[NV], nv[NV];
@@ -519,20 +504,99 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
             pnu[v] = nu[v];
             pnv[v] = nv[v];
             u[v] = same_row ? nu[v] : ring[next][v];
-            if constexpr (!ONE)
-              vv[v] = same_col ? nv[v] : vl[v];
-            else if constexpr (TAIL)
-              vv[v] = (c + j < len) ? nv[v] : vv[v];  // steps past the end change nothing
-            else
-              vv[v] = nv[v];
+            vv[v] = same_col ? nv[v] : vl[v];
           }
           x64 = x64n;
-          if constexpr (!ONE) {
-            ccur = ncol;
-            waddr = naddr;
-            ncol = col2;
-            naddr = naddr2;
+          ccur = ncol;
+          waddr = naddr;
+          ncol = col2;
+          naddr = naddr2;
+          pin();
+        }
+        decode(Wn1, c + CH);
+        Wn1 = Wn2;
+      };
+
+      // Folded step of a one-column block in which no row repeats in
+      // consecutive ratings (every block of a heavy item's own
+      // column-block, with cut points of unequal blocks).  The next rating
+      // has another row u' and the same column, so its partial products are
+      //   x'/KPL - u'.(v + d_v + (a e) u) = [x'/KPL - u'.(v + d_v)] - e [u'.(a u)]
+      // with d_v = -(a b) v: both brackets are known before e, and the
+      // dependency chain of a rating shrinks to the reduction, the lane read
+      // and one fma.  v stays in registers for the whole block and goes back
+      // to its LDS slot at the end.  The stored u and v are updated exactly
+      // as in the general step; only the rounding of the next dot product
+      // differs.  tcur: partial products of the current rating.
+      float tcur = 0.0f;
+      auto chunk_fold = [&](auto tail_tag, int32_t c) {
+        constexpr bool TAIL = decltype(tail_tag)::value;
+        const uint2 Wn2 = rp[c + 2 * CH + lane];
+#pragma unroll
+        for (int j = 0; j < CH; ++j) {
+          const int slot = (j == 0) ? CH - 1 : j - 1;
+          const int next = (j + 1) % CH;
+          float t = tcur;
+          pin();
+          t = t + dpp_mov<0xB1>(t);  // quad_perm [1,0,3,2]
+          pin();
+          if constexpr (TAIL)
+            st_row<NV, 0>(pnu, Ures, doff + ((c + j - 1 < len) ? prow : kOff), 0);
+          else
+            st_row<NV, 0>(pnu, Ures, doff, prow);
+          pin();
+          ringrow[slot] = rl(wrow, slot + D - (j == 0 ? CH : 0));
+          pin();
+          t = t + dpp_mov<0x4E>(t);  // quad_perm [2,3,0,1]
+          pin();
+          float du[NV], dv[NV];
+#pragma unroll
+          for (int v = 0; v < NV; ++v) du[v] = nab * u[v];
+          const uint32_t x64n = rl(__float_as_uint(wx), j + 1);  // the next rating's x
+          pin();
+          t = t + dpp_mov<0x141>(t);  // row_half_mirror
+          pin();
+#pragma unroll
+          for (int v = 0; v < NV; ++v) dv[v] = nab * vv[v];
+          pin();
+          ld_row<NV, 0>(ring[slot], Ures, doff, ringrow[slot]);
+          pin();
+          t = t + dpp_mov<0x140>(t);  // row_mirror
+          pin();
+          // the next rating's partial products before e (A) and the
+          // coefficient of -e (B)
+          float au[NV];
+          float A = __uint_as_float(x64n);
+#pragma unroll
+          for (int v = 0; v < NV; ++v) {
+            au[v] = alpha * u[v];
+            A = fmaf(-ring[next][v], vv[v] + dv[v], A);
           }
+          pin();
+          if constexpr (KPL >= 32) t = t + dpp_mov<0x142>(t);  // row_bcast:15
+          pin();
+          float B = ring[next][0] * au[0];
+#pragma unroll
+          for (int v = 1; v < NV; ++v) B = fmaf(ring[next][v], au[v], B);
+          pin();
+          if constexpr (KPL >= 64) t = t + dpp_mov<0x143>(t);  // row_bcast:31
+          pin();
+          const float e = __uint_as_float(rl(__float_as_uint(t), 63));
+          pin();
+          tcur = fmaf(-e, B, A);
+          const float ae = alpha * e;
+#pragma unroll
+          for (int v = 0; v < NV; ++v) {
+            const float nu = u[v] + fmaf(ae, vv[v], du[v]);
+            const float nv = vv[v] + fmaf(ae, u[v], dv[v]);
+            pnu[v] = nu;
+            u[v] = ring[next][v];
+            if constexpr (TAIL)
+              vv[v] = (c + j < len) ? nv : vv[v];  // steps past the end change nothing
+            else
+              vv[v] = nv;
+          }
+          prow = ringrow[j];
           pin();
         }
         decode(Wn1, c + CH);
@@ -543,14 +607,17 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
       // partial chunk they belong to a step past the end (its u store is
       // dropped, its v store lands in the spare slot).
       const int32_t full = len & ~(CH - 1);
-      if (ncols == 1 && P.single_col) {
-        for (int32_t c = 0; c < full; c += CH) chunk(std::false_type{}, std::true_type{}, c);
-        if (full < len) chunk(std::true_type{}, std::true_type{}, full);
+      if (fold) {
+        tcur = __uint_as_float(x64);
+#pragma unroll
+        for (int v = 0; v < NV; ++v) tcur = fmaf(-u[v], vv[v], tcur);
+        for (int32_t c = 0; c < full; c += CH) chunk_fold(std::false_type{}, c);
+        if (full < len) chunk_fold(std::true_type{}, full);
         if (full == len) st_row<NV, 0>(pnu, Ures, doff, prow);
         lds_st<NV>(vv, waddr);
       } else {
-        for (int32_t c = 0; c < full; c += CH) chunk(std::false_type{}, std::false_type{}, c);
-        if (full < len) chunk(std::true_type{}, std::false_type{}, full);
+        for (int32_t c = 0; c < full; c += CH) chunk(std::false_type{}, c);
+        if (full < len) chunk(std::true_type{}, full);
         if (full == len) st_row<NV, 0>(pnu, Ures, doff, prow);
         lds_st<NV>(pnv, pwaddr);
       }
@@ -786,6 +853,8 @@ const void *sgd_kernel(int kp, bool mask, int vmode) {
 }  // namespace
 
 size_t sgd_gv_lds_per_wave(int kp) { return (size_t)kPrefetch * kp * sizeof(float); }
+
+size_t sgd_lds_per_wave(int kp, int cols_max) { return (size_t)(cols_max + 1) * kp * sizeof(float); }
 
 hipError_t sgd_set_lds_limit(int kp, bool mask, int vmode, size_t lds_bytes) {
   const void *f = sgd_kernel(kp, mask, vmode);

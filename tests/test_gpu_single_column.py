@@ -1,14 +1,19 @@
-"""Blocks of a one-column column-block (BGMF_OPT_SINGLE_COLUMN): the sweep
-that keeps that column's v in registers through the block gives the same bits
-as the general step, and matches the oracle's epoch (Algorithm 1, Eq. 2-3)
-on the same layout.
+"""Blocks of a one-column column-block (BGMF_OPT_SINGLE_COLUMN).  A block in
+which no row repeats in consecutive ratings takes the folded step (v in
+registers for the whole block, the next rating's partial products formed
+before e is known): the stored u and v are updated as in the general step,
+only the rounding of the next dot product differs, so it must match the
+oracle's epoch (Algorithm 1, Eq. 2-3) on the same layout within the parity
+tolerance.  A block that repeats a row (a duplicate rating) takes the
+general step, so with every one-column block holding a duplicate the option
+changes no bit.
 
 The crafted workload puts one heavy column alone in each of the first three
-column-blocks (every user rates it) and plants what the register path must
-still get right: a duplicate rating whose two copies straddle a chunk
-boundary (the first rating of a chunk repeats the row before it, so u is
-forwarded), a duplicate inside a chunk, blocks whose length is not a multiple
-of the chunk, and a column-block with many columns beside them.
+column-blocks (every user rates it) and plants duplicates: one whose two
+copies straddle a chunk boundary, one inside a chunk, in some row-blocks
+only (those blocks take the general step, the others fold), blocks whose
+length is not a multiple of the chunk, and a column-block with many columns
+beside them.
 """
 import os
 
@@ -29,17 +34,20 @@ class _W:
     pass
 
 
-def _crafted(k, seed=7):
+def _crafted(k, seed=7, dup_all=False):
     """n users, heavy columns 0, 1, 2 in column-blocks of their own, the other
     columns in the last block; duplicates of rows 15 (copies at block
     positions 15 and 16) and 40 in every heavy column, and of row 520 of
-    column 1 (second row-block)."""
+    column 1 (second row-block).  ``dup_all``: also a duplicate in every
+    row-block of every heavy column."""
     n, m, p = 2_000, 61, 4
     rng = np.random.default_rng(seed)
     rows, cols = [], []
     for j in (0, 1, 2):
         r = np.arange(n)
         r = np.sort(np.r_[r, 15, 40, 520 if j == 1 else 41])
+        if dup_all:
+            r = np.sort(np.r_[r, 600, 1100, 1700])
         rows.append(r)
         cols.append(np.full(len(r), j))
     extra = 30_000
@@ -112,37 +120,81 @@ def test_crafted_layout_has_the_planted_cases():
     assert any(x % 16 for x in one)
 
 
-@pytest.mark.parametrize("k", [16, 48, 64, 128])
-@pytest.mark.parametrize("schedule", [0, 1])
-def test_crafted_same_bits_and_oracle(k, schedule):
-    w, rc, cc = _crafted(k)
-    on = _gpu(w, rc, cc, 1, schedule=schedule)
-    off = _gpu(w, rc, cc, 0, schedule=schedule)
-    assert np.array_equal(on[0], off[0]) and np.array_equal(on[1], off[1])
-    assert on[2] == off[2]
-    o = _oracle(w, rc, cc)
-    assert row_rel_err(on[0], o[0]) <= TOL and row_rel_err(on[1], o[1]) <= TOL
-    for a, b in zip(on[2], o[2]):
+def _check_oracle(g, o):
+    assert row_rel_err(g[0], o[0]) <= TOL and row_rel_err(g[1], o[1]) <= TOL
+    for a, b in zip(g[2], o[2]):
         assert abs(a - b) <= TOL * b
 
 
-def test_crafted_passes():
-    w, rc, cc = _crafted(64)
-    on = _gpu(w, rc, cc, 1, epochs=1, passes=3)
-    off = _gpu(w, rc, cc, 0, epochs=1, passes=3)
-    assert np.array_equal(on[0], off[0]) and np.array_equal(on[1], off[1])
-    o = _oracle(w, rc, cc, epochs=1, passes=3)
-    assert row_rel_err(on[0], o[0]) <= TOL and row_rel_err(on[1], o[1]) <= TOL
+@pytest.mark.parametrize("k", [16, 48, 64, 128])
+@pytest.mark.parametrize("schedule", [0, 1])
+def test_crafted_fold_and_oracle(k, schedule):
+    w, rc, cc = _crafted(k)
+    o = _oracle(w, rc, cc)
+    _check_oracle(_gpu(w, rc, cc, 1, schedule=schedule), o)
+    _check_oracle(_gpu(w, rc, cc, 0, schedule=schedule), o)
 
 
-def test_balanced_heavy_items_same_bits():
-    """Zipf items with nnz-balanced cut points (heavy items isolated); the
-    register path is taken (the general step is slower on one column)."""
-    from paper_2304_13724_amd import bgmf
-    w = make_config("large", n=48_000, m=1_800, nnz=1_000_000, p=128)
-    rc, cc = bgmf.bgmf_balanced_cuts(w.n, w.m, w.p, w.rows, w.cols, 65536, 64)
-    assert int(np.diff(cc).min()) == 1  # some column-blocks hold one item
+@pytest.mark.parametrize("k", [16, 64, 128])
+def test_repeated_rows_take_the_general_step(k):
+    w, rc, cc = _crafted(k, dup_all=True)
     on = _gpu(w, rc, cc, 1)
     off = _gpu(w, rc, cc, 0)
     assert np.array_equal(on[0], off[0]) and np.array_equal(on[1], off[1])
     assert on[2] == off[2]
+    _check_oracle(on, _oracle(w, rc, cc))
+
+
+def test_crafted_passes():
+    w, rc, cc = _crafted(64)
+    o = _oracle(w, rc, cc, epochs=1, passes=3)
+    for single in (1, 0):
+        g = _gpu(w, rc, cc, single, epochs=1, passes=3)
+        assert row_rel_err(g[0], o[0]) <= TOL and row_rel_err(g[1], o[1]) <= TOL
+
+
+def test_balanced_heavy_items_oracle():
+    """Zipf items with nnz-balanced cut points (heavy items isolated, their
+    blocks take the folded step), two epochs against the oracle."""
+    from paper_2304_13724_amd import bgmf
+    w = make_config("large", n=48_000, m=1_800, nnz=1_000_000, p=128)
+    rc, cc = bgmf.bgmf_balanced_cuts(w.n, w.m, w.p, w.rows, w.cols, 65536, 64)
+    assert int(np.diff(cc).min()) == 1  # some column-blocks hold one item
+    _check_oracle(_gpu(w, rc, cc, 1), _oracle(w, rc, cc))
+
+
+def test_fold_correction_term_is_exercised():
+    """One column rated by every user, factors drawn wide and a large step,
+    so that the term carried by the folded step (e times a u'.u) is several
+    percent of the next error: a wrong or missing term would miss the
+    oracle by far more than the tolerance."""
+    n, m, k, p = 3_000, 8, 64, 4
+    rng = np.random.default_rng(31)
+    rows = np.r_[np.arange(n), rng.integers(0, n, 4_000)].astype(np.int32)
+    cols = np.r_[np.zeros(n, np.int64), rng.integers(1, m, 4_000)].astype(np.int32)
+    order = rng.permutation(len(rows))
+    w = _W()
+    w.n, w.m, w.k, w.p = n, m, k, p
+    w.rows, w.cols = rows[order], cols[order]
+    w.vals = rng.integers(1, 6, len(rows)).astype(np.float32)
+    w.U0 = rng.normal(0.0, 0.3, (n, k)).astype(np.float32)
+    w.V0 = rng.normal(0.0, 0.3, (m, k)).astype(np.float32)
+    w.alpha, w.beta = 0.05, 0.05
+    rc = np.array([(R * n + p - 1) // p for R in range(p + 1)], dtype=np.int64)
+    cc = np.array([0, 1, 2, 3, m], dtype=np.int64)
+    # size of the folded term along the first block of column 0 (rows in
+    # ascending order), in binary64 with the plain update
+    U = w.U0.astype(np.float64)
+    v = w.V0[0].astype(np.float64)
+    x = np.zeros(n)
+    x[rows[:n]] = w.vals[np.argsort(order)][:n]
+    ratio = 0.0
+    for i in range(rc[1] - 1):
+        e = x[i] - U[i] @ v
+        u = U[i].copy()
+        U[i] += w.alpha * (e * v - w.beta * U[i])
+        v += w.alpha * (e * u - w.beta * v)
+        ratio = max(ratio, abs(e * w.alpha * (U[i + 1] @ u)) / (abs(x[i + 1] - U[i + 1] @ v) + 1e-3))
+    assert ratio > 0.05
+    o = _oracle(w, rc, cc)
+    _check_oracle(_gpu(w, rc, cc, 1), o)
