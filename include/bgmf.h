@@ -243,12 +243,27 @@ int bgmf_factor_ptrs(bgmf_t *h, float **U_dev, float **V_dev);
 #define BGMF_OPT_SINGLE_COLUMN 11 /* 1 (default): with V staged in LDS, a block
                                     whose column-block is one column wide (a heavy
                                     item given a column-block of its own through
-                                    bgmf_set_cuts) keeps that column's v in
-                                    registers from its first rating to its last,
-                                    instead of a write and a read of LDS per
-                                    rating; 0: such blocks take the general step.
-                                    The arithmetic is the same, so the results are
-                                    bit-identical. */
+                                    bgmf_set_cuts) and whose consecutive ratings
+                                    never share a row keeps that column's v in
+                                    registers from its first rating to its last
+                                    and forms each rating's partial products
+                                    before the previous error is known (a shorter
+                                    dependency chain); 0: such blocks take the
+                                    general step.  The stored updates are the same
+                                    formula, the next dot product rounds
+                                    differently, so results differ in the last
+                                    bits (both match the exact sequential
+                                    schedule within the parity tolerance). */
+#define BGMF_OPT_LDS_HANDOVER 12 /* 1 (default): with V staged in LDS and one
+                                    persistent launch, the waves of a workgroup
+                                    (consecutive row-blocks) pass column slices
+                                    to each other through LDS; only slices that
+                                    enter or leave the workgroup, and all of them
+                                    after a launch, go through global memory.
+                                    Used when the larger LDS ring still lets every
+                                    wave be resident.  0: every hand-over goes
+                                    through global memory.  Same arithmetic, so
+                                    the results are bit-identical. */
 int bgmf_set_option(bgmf_t *h, int32_t option, int64_t value);
 int bgmf_get_option(const bgmf_t *h, int32_t option, int64_t *value);
 

@@ -37,6 +37,7 @@ BGMF_OPT_STREAM_CHUNKS = 8
 BGMF_OPT_RESIDENT_STRATA = 9
 BGMF_OPT_BLOCK_PASSES = 10
 BGMF_OPT_SINGLE_COLUMN = 11
+BGMF_OPT_LDS_HANDOVER = 12
 
 EXPORTED = (
     "bgmf_create", "bgmf_destroy", "bgmf_last_error", "bgmf_set_stream", "bgmf_set_factors",

@@ -45,11 +45,12 @@ struct bgmf {
   size_t lds_limit = 0;
   bool lds_fits = false;
   int wpg_lds = 1, wpg_gv = kWavesPerGroup;
+  int lds_ring = 0;  // areas of the LDS hand-over ring (0: none)
   size_t lds_bytes_lds = 0, lds_bytes_gv = 0;
   bool coop_lds = false, coop_gv = false;
   // options
   int64_t schedule = 0, wait_us = 10000000, xcd_remap = 1, v_staging = 0, passes = 1;
-  int64_t single_col = 1;
+  int64_t single_col = 1, lds_handover = 1;
   // timing
   hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
   bool epoch_timed = false, rmse_timed = false;
@@ -165,17 +166,30 @@ hipError_t configure_sweep(bgmf_t *h) {
   hipError_t e;
   for (int vm : {kVLds, kVGlobal, kVGlobalCoherent})
     if ((e = sgd_set_lds_limit(h->kp, mask, vm, h->lds_limit)) != hipSuccess) return e;
-  const size_t slice = sgd_lds_per_wave(h->kp, h->cols_max);
   h->wpg_lds = kWavesPerGroup;
-  while (h->wpg_lds > 1 && h->wpg_lds * slice > h->lds_limit) h->wpg_lds >>= 1;
-  h->lds_bytes_lds = h->wpg_lds * slice;
+  while (h->wpg_lds > 1 && sgd_lds_bytes(h->kp, h->cols_max, h->wpg_lds, 0) > h->lds_limit)
+    h->wpg_lds >>= 1;
+  h->lds_ring = 0;
+  h->lds_bytes_lds = sgd_lds_bytes(h->kp, h->cols_max, h->wpg_lds, 0);
   h->lds_fits = h->lds_bytes_lds <= h->lds_limit;
   h->coop_lds = false;
+  const int64_t groups = (p + h->wpg_lds - 1) / h->wpg_lds;
   if (h->lds_fits) {
     if ((e = sgd_occupancy(h->kp, mask, kVLds, h->wpg_lds, h->lds_bytes_lds, &per_cu)) !=
         hipSuccess)
       return e;
-    h->coop_lds = (int64_t)per_cu * h->cus >= (p + h->wpg_lds - 1) / h->wpg_lds;
+    h->coop_lds = (int64_t)per_cu * h->cus >= groups;
+    // hand-over ring of twice the workgroup's waves, if every wave can
+    // still be resident with it
+    const int ring = 2 * h->wpg_lds;
+    const size_t rb = sgd_lds_bytes(h->kp, h->cols_max, h->wpg_lds, ring);
+    if (h->coop_lds && h->lds_handover && h->wpg_lds > 1 && rb <= h->lds_limit) {
+      if ((e = sgd_occupancy(h->kp, mask, kVLds, h->wpg_lds, rb, &per_cu)) != hipSuccess) return e;
+      if ((int64_t)per_cu * h->cus >= groups) {
+        h->lds_ring = ring;
+        h->lds_bytes_lds = rb;
+      }
+    }
   }
   h->wpg_gv = kWavesPerGroup;
   h->lds_bytes_gv = h->wpg_gv * sgd_gv_lds_per_wave(h->kp);
@@ -638,6 +652,7 @@ int bgmf_epoch(bgmf_t *h, float alpha, float beta) {
   P.single_col = (int32_t)h->single_col;
   P.rowrep = h->rowrep;
   const SweepShape sh = sweep_shape(h);
+  P.lds_ring = sh.lds ? h->lds_ring : 0;
   HIP_TRY(h, hipEventRecord(h->ev[0], h->stream));
   if (h->ooc) {
     // resident strata, then the streamed chunks; each range is one
@@ -982,6 +997,11 @@ int bgmf_set_option(bgmf_t *h, int32_t option, int64_t value) {
       if (value != 0 && value != 1) return fail(h, BGMF_E_ARG, "single column must be 0 or 1");
       h->single_col = value;
       return BGMF_OK;
+    case BGMF_OPT_LDS_HANDOVER:
+      if (value != 0 && value != 1) return fail(h, BGMF_E_ARG, "LDS hand-over must be 0 or 1");
+      h->lds_handover = value;
+      HIP_TRY(h, configure_sweep(h));
+      return BGMF_OK;
     case BGMF_OPT_STREAM_CHUNKS:
       return fail(h, BGMF_E_ARG, "BGMF_OPT_STREAM_CHUNKS is read-only");
     case BGMF_OPT_RESIDENT_STRATA:
@@ -1006,6 +1026,7 @@ int bgmf_get_option(const bgmf_t *h, int32_t option, int64_t *value) {
     case BGMF_OPT_RESIDENT_STRATA: *value = h->ooc ? h->s_res : h->p; return BGMF_OK;
     case BGMF_OPT_BLOCK_PASSES: *value = h->passes; return BGMF_OK;
     case BGMF_OPT_SINGLE_COLUMN: *value = h->single_col; return BGMF_OK;
+    case BGMF_OPT_LDS_HANDOVER: *value = h->lds_handover; return BGMF_OK;
     case BGMF_OPT_PLACEMENT: {
       const SweepShape sh = sweep_shape(h);
       *value = (sh.lds ? 1 : 2) | (sh.persistent ? 4 : 0);

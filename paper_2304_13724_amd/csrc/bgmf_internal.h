@@ -76,6 +76,8 @@ struct SgdParams {
   int32_t single_col;        // 1: blocks of a one-column column-block keep v in registers
   const uint8_t *rowrep;     // [p * p], slot s*p + b: 1 if two consecutive ratings of the
                              // block share a row
+  int32_t lds_ring;          // LDS sweep, persistent launches: areas in the workgroup's
+                             // hand-over ring (0: each wave its own area, global hand-over)
 };
 constexpr int kFlagStride = 16;  // int64 words per flag (one 128-byte line)
 constexpr int kWavesPerGroup = 4;
@@ -97,8 +99,11 @@ hipError_t sgd_occupancy(int kp, bool mask, int vmode, int waves_per_group, size
                          int *groups_per_cu);
 hipError_t sgd_set_lds_limit(int kp, bool mask, int vmode, size_t lds_bytes);
 size_t sgd_gv_lds_per_wave(int kp);
-// LDS of one wave of the LDS sweep: cols_max + 1 column slots.
+// LDS of one area of the LDS sweep: cols_max + 1 column slots.  A workgroup
+// of w waves needs sgd_lds_bytes(kp, cols_max, w, ring): w areas (ring = 0)
+// or a hand-over ring of `ring` areas, and one progress word per wave.
 size_t sgd_lds_per_wave(int kp, int cols_max);
+size_t sgd_lds_bytes(int kp, int cols_max, int waves_per_group, int ring);
 
 hipError_t launch_rmse(const uint2 *rec, const int64_t *wblock_ptr, const float *U,
                        const float *V, const Grid &G, int64_t rows_max, int32_t k, int64_t nnz,

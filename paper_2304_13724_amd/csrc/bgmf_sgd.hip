@@ -200,6 +200,23 @@ __device__ __forceinline__ bool wait_progress(const int64_t *flag, int64_t targe
   return true;
 }
 
+// Wait until an LDS progress word of this workgroup is >= target.  LDS
+// accesses of one wave complete in order and the writer stored the word
+// after its slice accesses had completed, so the slice reads that follow
+// see the slice.  Returns false on timeout.
+__device__ __forceinline__ bool wait_lds_progress(volatile __attribute__((address_space(3))) int64_t *w,
+                                                  int64_t target, int64_t wait_ticks) {
+  if (*w < target) {
+    const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+    while (*w < target) {
+      __builtin_amdgcn_s_sleep(1);
+      if ((int64_t)(__builtin_amdgcn_s_memrealtime() - t0) > wait_ticks) return false;
+    }
+  }
+  asm volatile("" ::: "memory");
+  return true;
+}
+
 // Publish progress: all earlier stores of the wave (the column slice) have
 // completed before the progress word is written.
 __device__ __forceinline__ void publish_progress(int64_t *flag, int64_t value) {
@@ -276,8 +293,8 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
   static_assert((CH & (CH - 1)) == 0 && CH <= 32,
                 "full chunks are counted with a mask; lanes j + D stay in the 64-record window");
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
+  const int wpg = (int)(blockDim.x >> 6);
   const int b = row_block_of_wave(P, wave);
-  if (b >= P.p) return;
   const L ln(P.k);
   const int lane = ln.lane;
   const uint32_t doff = ln.doff;
@@ -287,16 +304,37 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
   const int k = P.k;
   const uint32_t rowbytes = (uint32_t)k * 4u;
   const uint32_t colbytes = (uint32_t)KP * 4u;
+  char *ldsb = reinterpret_cast<char *>(lds);
+
+  // Column slices live in LDS areas of cols_max + 1 slots.  Without the
+  // hand-over ring each wave has its own area.  With it (persistent
+  // launches), the workgroup's waves, which own consecutive row-blocks,
+  // share a ring of R areas: the slice that wave w finishes in stratum s is
+  // the one wave w - 1 needs in stratum s + 1, so it stays in its area
+  // (index (w + s) mod R, the same along the slice's way through the
+  // workgroup) and moves on with an LDS progress word instead of a
+  // device-scope write-back, completion wait and reload.  Only the slices
+  // entering the workgroup (at its last wave) and leaving it (at wave 0, and
+  // every slice after the launch's last stratum) go through global memory.
+  const bool lho = P.lds_ring > 0 && P.s_end - P.s_begin > 1;
+  const int R = lho ? P.lds_ring : wpg;
+  const uint32_t areabytes = (uint32_t)(P.cols_max + 1) * colbytes;
+  using lds_i64 = __attribute__((address_space(3))) int64_t;
+  volatile lds_i64 *const lprog = (volatile lds_i64 *)((lds_char *)ldsb + (uint32_t)R * areabytes);
+  if (lho) {
+    // strata completed by each wave, as the global progress words count them
+    if (b < P.p && lane == 0) lprog[wave] = P.g_base + P.s_begin;
+    __syncthreads();
+  }
+  if (b >= P.p) return;
 
   // U rows of row-block b (owned by this wave for the whole launch)
   const int64_t r0 = G.row_start(b);
   const uint32_t rows_b = (uint32_t)(G.row_start(b + 1) - r0);
   const __amdgpu_buffer_rsrc_t Ures =
       __builtin_amdgcn_make_buffer_rsrc(P.U + r0 * k, (short)0, (int)(rows_b * rowbytes), kBufWord3);
-  // this wave's LDS column slots: cols_max real ones and one spare
-  const uint32_t vbase = ((uint32_t)wave * (P.cols_max + 1) * KP + ln.first) * 4u;
+  // in an LDS area: cols_max real column slots and one spare
   const uint32_t spare = (uint32_t)P.cols_max * colbytes;
-  char *ldsb = reinterpret_cast<char *>(lds);
   const int64_t *blk_b = P.blk + (int64_t)b * P.stride_b;
   // alpha is kept in a VGPR so that alpha * e (e is a scalar) is one instruction
   float alpha;
@@ -323,6 +361,13 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
     const uint2 *rp = P.rec + (beg - P.rec_origin);
     const bool fold = ncols == 1 && P.single_col &&
                       __builtin_amdgcn_readfirstlane(P.rowrep[(int64_t)s * P.p + b]) == 0;
+    // this lane's part of the LDS area holding column-block C; whether the
+    // slice comes from wave w + 1 of this workgroup (through LDS) and goes
+    // on to wave w - 1 (through LDS)
+    const int area = lho ? (wave + s) % R : wave;
+    const uint32_t vbase = (uint32_t)area * areabytes + ln.first * 4u;
+    const bool from_lds = lho && s > P.s_begin && wave + 1 < wpg && b + 1 < P.p;
+    const bool to_lds = lho && s + 1 < P.s_end && wave > 0;
 
     // Decoded window of 64 records starting at chunk position c:
     //   wrow = byte offset of the row in U (row 0 past the block end, so the
@@ -353,19 +398,30 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
       }
     };
     if (len > 0) prime();
+    const bool stage = !from_lds && (len > 0 || to_lds);
     if (s > P.s_begin) {
       // column-block C was last updated by row-block b+1 in stratum g-1
-      const int nb = (b + 1 == P.p) ? 0 : b + 1;
-      if (!wait_progress(P.flags + (int64_t)nb * kFlagStride, g, P.wait_ticks)) {
+      bool ok;
+      if (from_lds) {
+        ok = wait_lds_progress(lprog + wave + 1, g, P.wait_ticks);
+      } else {
+        const int nb = (b + 1 == P.p) ? 0 : b + 1;
+        ok = wait_progress(P.flags + (int64_t)nb * kFlagStride, g, P.wait_ticks);
+        // the area's previous slice (position wave + s - R in the ring) must
+        // have left the workgroup: wave 0 finished its stratum wave + s - R
+        if (ok && lho && stage && wave + s - R >= P.s_begin)
+          ok = wait_lds_progress(lprog, g + wave - R + 1, P.wait_ticks);
+      }
+      if (!ok) {
         __hip_atomic_store(P.err, kErrTimeout, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         return;
       }
     }
-    if (len > 0) {
+    const __amdgpu_buffer_rsrc_t Vres = __builtin_amdgcn_make_buffer_rsrc(
+        P.V + c0 * k, (short)0, (int)((uint32_t)ncols * rowbytes), kBufWord3);
+    if (stage) {
       // stage the column slice of V in LDS, 16 columns per round trip
       // (columns past the slice read 0 and land in the spare slot)
-      const __amdgpu_buffer_rsrc_t Vres = __builtin_amdgcn_make_buffer_rsrc(
-          P.V + c0 * k, (short)0, (int)((uint32_t)ncols * rowbytes), kBufWord3);
       for (int cb = 0; cb < ncols; cb += 16) {
         float tmp[16][NV];
 #pragma unroll
@@ -375,6 +431,8 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
         for (int i = 0; i < 16; ++i)
           lds_st<NV>(tmp[i], ldsb, vbase + (uint32_t)min(cb + i, P.cols_max) * colbytes);
       }
+    }
+    if (len > 0) {
       // GPU_STEPS passes over the block, its ratings in the same order each
       // time (Section 1.3); a later pass re-reads the U rows this wave
       // stored in the previous one (the hardware keeps a wave's accesses to
@@ -622,7 +680,9 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
         lds_st<NV>(pnv, pwaddr);
       }
       }
-      // publish the column slice, 16 columns per round (stores past the
+    }
+    if (!to_lds && (len > 0 || from_lds)) {
+      // write the column slice back, 16 columns per round (stores past the
       // slice are dropped)
       for (int cb = 0; cb < ncols; cb += 16) {
         float tmp[16][NV];
@@ -636,7 +696,14 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
     }
     // a launch of one stratum is ordered by the kernel boundary instead;
     // every lane publishes its own stores (all write the same value)
-    if (P.s_end - P.s_begin > 1) publish_progress(P.flags + (int64_t)b * kFlagStride, g + 1);
+    if (P.s_end - P.s_begin > 1 && !to_lds)
+      publish_progress(P.flags + (int64_t)b * kFlagStride, g + 1);
+    if (lho) {
+      // the slice's LDS writes (or the write-back's LDS reads) are done
+      // before the word moves; lane 0 writes it
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      if (lane == 0) lprog[wave] = g + 1;
+    }
   }
 }
 
@@ -855,6 +922,11 @@ const void *sgd_kernel(int kp, bool mask, int vmode) {
 size_t sgd_gv_lds_per_wave(int kp) { return (size_t)kPrefetch * kp * sizeof(float); }
 
 size_t sgd_lds_per_wave(int kp, int cols_max) { return (size_t)(cols_max + 1) * kp * sizeof(float); }
+
+size_t sgd_lds_bytes(int kp, int cols_max, int waves_per_group, int ring) {
+  const size_t areas = ring > 0 ? (size_t)ring : (size_t)waves_per_group;
+  return areas * sgd_lds_per_wave(kp, cols_max) + (size_t)waves_per_group * sizeof(int64_t);
+}
 
 hipError_t sgd_set_lds_limit(int kp, bool mask, int vmode, size_t lds_bytes) {
   const void *f = sgd_kernel(kp, mask, vmode);
