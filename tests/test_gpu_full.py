@@ -4,6 +4,9 @@ bench.py times (persistent schedule, default options).
 * 100M ratings, k=64, p=1024: bucketing bit-exact against the oracle; U, V
   and RMSE after one epoch within 1e-4 of the oracle's multithreaded epoch
   (bit-identical to its sequential one).
+* The 100M workload with nnz-balanced cut points (heavy items on their own
+  column-blocks, the folded one-column step): bucketing bit-exact, one
+  epoch within 1e-4 of the oracle and as close to binary64 as the oracle.
 * 10M ratings, k=32, p=256: three epochs, RMSE after each and final U, V.
 * 250M ratings, k=128, p=2048 (column slices of 306 x 128 floats, so V
   stays in global memory): bucketing bit-exact; the global-memory sweep
@@ -75,6 +78,41 @@ def test_large_one_epoch_parity(large):
     assert row_rel_err(g[2], o[2]) <= TOL
     assert row_rel_err(g[3], o[3]) <= TOL
     assert abs(g[4][0] - o[4][0]) <= TOL * o[4][0]
+
+
+def test_large_balanced_blocks_one_epoch(large):
+    """The same workload with nnz-balanced cut points (bench.py's balanced
+    variant): every heavy item has a column-block of its own, so the longest
+    chains run through the folded one-column step.  Bucketing bit-exact
+    against the oracle's cut bucketing; U, V and RMSE within 1e-4 of the
+    oracle, and no further from the binary64 epoch than 1.5 times the
+    oracle's own distance."""
+    from paper_2304_13724_amd import bgmf
+    w = large[0]
+    rc, cc = bgmf.bgmf_balanced_cuts(w.n, w.m, w.p, w.rows, w.cols, 65536, 64)
+    with bgmf.Model(w.n, w.m, w.k, w.p) as mdl:
+        mdl.set_cuts(rc, cc)
+        mdl.set_factors(w.U0, w.V0)
+        mdl.load_coo(w.rows, w.cols, w.vals)
+        bp, perm = mdl.get_layout()
+        mdl.epoch(w.alpha, w.beta)
+        r = mdl.rmse()
+        U, V = mdl.get_factors()
+    obp, operm = oracle.bucket_cuts(w.n, w.m, w.p, rc, cc, w.rows, w.cols)
+    assert np.array_equal(bp, obp) and np.array_equal(perm, operm)
+    Uo, Vo = w.U0.copy(), w.V0.copy()
+    oracle.epoch_mt(w.p, w.rows, w.cols, w.vals, obp, operm, Uo, Vo, w.alpha, w.beta, THREADS)
+    ro = oracle.rmse(w.rows, w.cols, w.vals, Uo, Vo)
+    d_go = max(row_rel_err(U, Uo), row_rel_err(V, Vo))
+    U64, V64 = w.U0.astype(np.float64), w.V0.astype(np.float64)
+    oracle.epoch_f64(w.p, w.rows, w.cols, w.vals, obp, operm, U64, V64, w.alpha, w.beta, THREADS)
+    d_o64 = max(row_rel_err(Uo, U64), row_rel_err(Vo, V64))
+    d_g64 = max(row_rel_err(U, U64), row_rel_err(V, V64))
+    print(f"balanced blocks: rmse gpu {r:.9f} oracle {ro:.9f}; row rel err gpu-oracle {d_go:.3e}, "
+          f"oracle-f64 {d_o64:.3e}, gpu-f64 {d_g64:.3e}", flush=True)
+    assert abs(r - ro) <= TOL * ro
+    assert d_go <= TOL
+    assert d_g64 <= 1.5 * d_o64
 
 
 def test_medium_three_epochs():
