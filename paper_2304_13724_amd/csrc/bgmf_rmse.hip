@@ -240,8 +240,13 @@ __global__ void k_zero(double *x, int64_t count) {
 }
 
 // Variant with the row-block's U rows staged in LDS: one workgroup of 16
-// waves per row-block, u_i read from LDS, v_j from global memory (L2).
-// Used when rows x k x 4 bytes fit in LDS.
+// waves per row-block, u_i read from LDS, v_j from global memory.  The
+// row-block's records of all strata are contiguous (wave-major), so each
+// wave sums one contiguous sixteenth of them as a single stream; a table of
+// block starts and column-blocks in LDS gives the block of each rating (a
+// lane group steps its block forward as its ratings cross block starts), so
+// no block boundary waits for memory.  Used when the rows and the tables
+// fit in LDS.
 constexpr int kLdsWaves = 16;
 
 template <int KP>
@@ -263,27 +268,50 @@ k_rmse_lds(const uint2 *__restrict__ rec, const int64_t *__restrict__ wblock_ptr
   const uint32_t rows_b = (uint32_t)(G.row_start(b + 1) - r0);
   const uint32_t rmax = rows_b - 1u;
   const int kq = k / 4;
+  // after the rows: the start of block (b, s) relative to the row-block's
+  // first record (p + 1 entries), then per stratum its column-block's first
+  // column and widest local column
+  int32_t *bnd = reinterpret_cast<int32_t *>(us + rows_b * (uint32_t)kq);
+  int2 *ctab = reinterpret_cast<int2 *>(bnd + ((p + 2) & ~1));
+  const int64_t W0 = wblock_ptr[(int64_t)b * p];
   {  // the row-block's rows are contiguous in U
     const float4 *src = reinterpret_cast<const float4 *>(U + r0 * k);
     const uint32_t total = rows_b * (uint32_t)kq;
     for (uint32_t i = threadIdx.x; i < total; i += blockDim.x) us[i] = src[i];
+    for (int s = threadIdx.x; s <= p; s += blockDim.x)
+      bnd[s] = (int32_t)(wblock_ptr[(int64_t)b * p + s] - W0);
+    for (int s = threadIdx.x; s < p; s += blockDim.x) {
+      const int C = (b + s) % p;
+      const int64_t c0 = G.col_start(C);
+      ctab[s] = make_int2((int32_t)c0, (int32_t)(G.col_start(C + 1) - c0 - 1));
+    }
   }
   __syncthreads();
+  const int32_t T = bnd[p];
+  const int32_t tb = (int32_t)((int64_t)T * wave / kLdsWaves);
+  const int32_t te = (int32_t)((int64_t)T * (wave + 1) / kLdsWaves);
   double acc = 0.0;
-  for (int s = wave; s < p; s += kLdsWaves) {
-    const int64_t beg = wblock_ptr[(int64_t)b * p + s];
-    const int64_t end = wblock_ptr[(int64_t)b * p + s + 1];
-    if (beg == end) continue;
-    const int C = (b + s) % p;
-    const float *Vb = V + G.col_start(C) * k;
-    const uint32_t cmax = (uint32_t)(G.col_start(C + 1) - G.col_start(C)) - 1u;
+  if (tb < te) {
+    // block of the wave's first rating: the last s with bnd[s] <= tb
+    int32_t lo = 0, hi = p - 1;
+    while (lo < hi) {
+      const int32_t mid = (lo + hi + 1) >> 1;
+      if (bnd[mid] <= tb) lo = mid;
+      else hi = mid - 1;
+    }
+    int32_t sg = lo;           // block of the lane group's current rating
+    int32_t nb = bnd[sg + 1];  // start of the block after it
+    int2 ct = ctab[sg];
+    const uint2 *rb = rec + W0;
+    // records of the next iteration are loaded one iteration ahead, so the
+    // factor-row loads never wait for a record load
     uint2 rn[UNR];
 #pragma unroll
     for (int u = 0; u < UNR; ++u) {
-      const int64_t t = beg + u * RPS + grp;
-      rn[u] = rec[t < end ? t : beg];
+      const int32_t t = tb + u * RPS + grp;
+      rn[u] = rb[t < te ? t : tb];
     }
-    for (int64_t t0 = beg; t0 < end; t0 += RPS * UNR) {
+    for (int32_t t0 = tb; t0 < te; t0 += RPS * UNR) {
       float4 a[UNR][QL], c[UNR][QL];
       float x[UNR];
       bool ok[UNR];
@@ -291,17 +319,23 @@ k_rmse_lds(const uint2 *__restrict__ rec, const int64_t *__restrict__ wblock_ptr
 #pragma unroll
       for (int u = 0; u < UNR; ++u) {
         r[u] = rn[u];
-        const int64_t t = t0 + RPS * UNR + u * RPS + grp;
-        rn[u] = rec[t < end ? t : beg];
+        const int32_t t = t0 + RPS * UNR + u * RPS + grp;
+        rn[u] = rb[t < te ? t : tb];
       }
 #pragma unroll
       for (int u = 0; u < UNR; ++u) {
-        const int64_t t = t0 + u * RPS + grp;
-        ok[u] = t < end;
+        const int32_t t = t0 + u * RPS + grp;
+        ok[u] = t < te;
+        // step to the block of rating t (past empty blocks); t < T = bnd[p]
+        while (ok[u] && t >= nb) {
+          ++sg;
+          nb = bnd[sg + 1];
+          ct = ctab[sg];
+        }
         x[u] = __uint_as_float(r[u].y);
         const uint32_t row = min(r[u].x & kRowMask, rmax);
-        const uint32_t col = min((r[u].x >> kColShift) & kColMask, cmax);
-        const float4 *vp = reinterpret_cast<const float4 *>(Vb + (int64_t)col * k);
+        const uint32_t col = min((r[u].x >> kColShift) & kColMask, (uint32_t)ct.y);
+        const float4 *vp = reinterpret_cast<const float4 *>(V + ((int64_t)ct.x + col) * k);
 #pragma unroll
         for (int i = 0; i < QL; ++i) {
           // branch-free: slices past k read slice 0 and are zeroed after
@@ -363,7 +397,8 @@ hipError_t launch_rmse_kp(const uint2 *rec, const int64_t *wblock_ptr, const flo
                           double *partials, size_t lds_limit, int64_t *count,
                           hipStream_t stream) {
   const int32_t p = G.p;
-  const size_t lds = (size_t)rows_max * (size_t)k * sizeof(float);
+  const size_t lds = (size_t)rows_max * (size_t)k * sizeof(float) +
+                     (size_t)((p + 2) & ~1) * sizeof(int32_t) + (size_t)p * sizeof(int2);
   if (lds <= lds_limit) {
     static bool attr_set = false;
     if (!attr_set) {
