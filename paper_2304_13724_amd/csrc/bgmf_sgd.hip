@@ -582,44 +582,66 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
       //   x'/KPL - u'.(v + d_v + (a e) u) = [x'/KPL - u'.(v + d_v)] - e [u'.(a u)]
       // with d_v = -(a b) v: both brackets are known before e, and the
       // dependency chain of a rating shrinks to the reduction, the lane read
-      // and one fma.  v stays in registers for the whole block and goes back
-      // to its LDS slot at the end.  The stored u and v are updated exactly
-      // as in the general step; only the rounding of the next dot product
-      // differs.  tcur: partial products of the current rating.
-      float tcur = 0.0f;
+      // and one fma.  The update of a rating's u and v (exactly the general
+      // step's formula) is then off that chain: it is done during the next
+      // rating's reduction, in its gaps, together with the store of u and
+      // the ring refill.  v stays in registers for the whole block and goes
+      // back to its LDS slot at the end; only the rounding of the next dot
+      // product differs from the general step.
+      //   tcur: partial products of the current rating t
+      //   ep, up, vp, dup, dvp, prow: e, u, v, the decay products and the row
+      //   of rating t - 1, whose update is still to be applied
+      //   uc: u of rating t
+      float tcur = 0.0f, ep = 0.0f;
+      float up[NV], vp[NV], dup[NV], dvp[NV], uc[NV];
       auto chunk_fold = [&](auto tail_tag, int32_t c) {
         constexpr bool TAIL = decltype(tail_tag)::value;
         const uint2 Wn2 = rp[c + 2 * CH + lane];
 #pragma unroll
         for (int j = 0; j < CH; ++j) {
-          const int slot = (j == 0) ? CH - 1 : j - 1;
-          const int next = (j + 1) % CH;
-          float t = tcur;
+          const int slot = (j == 0) ? CH - 1 : j - 1;  // ring slot of rating t - 1
+          const int next = (j + 1) % CH;               // ring slot of rating t + 1
+          // rating t - 1: increments of v and u
+          const float ae = alpha * ep;
+          float nvx[NV], nux[NV], vc[NV], nu[NV];
+#pragma unroll
+          for (int v = 0; v < NV; ++v) nvx[v] = fmaf(ae, up[v], dvp[v]);
           pin();
+          float t = tcur;
           t = t + dpp_mov<0xB1>(t);  // quad_perm [1,0,3,2]
           pin();
-          if constexpr (TAIL)
-            st_row<NV, 0>(pnu, Ures, doff + ((c + j - 1 < len) ? prow : kOff), 0);
-          else
-            st_row<NV, 0>(pnu, Ures, doff, prow);
-          pin();
           ringrow[slot] = rl(wrow, slot + D - (j == 0 ? CH : 0));
+          // v of rating t (rating t - 1's result; unchanged past the block end)
+#pragma unroll
+          for (int v = 0; v < NV; ++v) {
+            if constexpr (TAIL)
+              vc[v] = (c + j - 1 < len) ? vp[v] + nvx[v] : vp[v];
+            else
+              vc[v] = vp[v] + nvx[v];
+          }
           pin();
           t = t + dpp_mov<0x4E>(t);  // quad_perm [2,3,0,1]
           pin();
-          float du[NV], dv[NV];
 #pragma unroll
-          for (int v = 0; v < NV; ++v) du[v] = nab * u[v];
+          for (int v = 0; v < NV; ++v) nux[v] = fmaf(ae, vp[v], dup[v]);
           const uint32_t x64n = rl(__float_as_uint(wx), j + 1);  // the next rating's x
           pin();
           t = t + dpp_mov<0x141>(t);  // row_half_mirror
           pin();
+          float duc[NV], dvc[NV];
 #pragma unroll
-          for (int v = 0; v < NV; ++v) dv[v] = nab * vv[v];
-          pin();
-          ld_row<NV, 0>(ring[slot], Ures, doff, ringrow[slot]);
+          for (int v = 0; v < NV; ++v) {
+            nu[v] = up[v] + nux[v];
+            duc[v] = nab * uc[v];
+          }
           pin();
           t = t + dpp_mov<0x140>(t);  // row_mirror
+          pin();
+          ld_row<NV, 0>(ring[slot], Ures, doff, ringrow[slot]);
+#pragma unroll
+          for (int v = 0; v < NV; ++v) dvc[v] = nab * vc[v];
+          pin();
+          if constexpr (KPL >= 32) t = t + dpp_mov<0x142>(t);  // row_bcast:15
           pin();
           // the next rating's partial products before e (A) and the
           // coefficient of -e (B)
@@ -627,35 +649,36 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
           float A = __uint_as_float(x64n);
 #pragma unroll
           for (int v = 0; v < NV; ++v) {
-            au[v] = alpha * u[v];
-            A = fmaf(-ring[next][v], vv[v] + dv[v], A);
+            au[v] = alpha * uc[v];
+            A = fmaf(-ring[next][v], fmaf(nab, vc[v], vc[v]), A);
           }
           pin();
-          if constexpr (KPL >= 32) t = t + dpp_mov<0x142>(t);  // row_bcast:15
+          if constexpr (KPL >= 64) t = t + dpp_mov<0x143>(t);  // row_bcast:31
           pin();
           float B = ring[next][0] * au[0];
 #pragma unroll
           for (int v = 1; v < NV; ++v) B = fmaf(ring[next][v], au[v], B);
           pin();
-          if constexpr (KPL >= 64) t = t + dpp_mov<0x143>(t);  // row_bcast:31
-          pin();
           const float e = __uint_as_float(rl(__float_as_uint(t), 63));
           pin();
+          // rating t - 1's u (dropped past the block end)
+          if constexpr (TAIL)
+            st_row<NV, 0>(nu, Ures, doff + ((c + j - 1 < len) ? prow : kOff), 0);
+          else
+            st_row<NV, 0>(nu, Ures, doff, prow);
+          pin();
           tcur = fmaf(-e, B, A);
-          const float ae = alpha * e;
+          pin();
+          ep = e;
 #pragma unroll
           for (int v = 0; v < NV; ++v) {
-            const float nu = u[v] + fmaf(ae, vv[v], du[v]);
-            const float nv = vv[v] + fmaf(ae, u[v], dv[v]);
-            pnu[v] = nu;
-            u[v] = ring[next][v];
-            if constexpr (TAIL)
-              vv[v] = (c + j < len) ? nv : vv[v];  // steps past the end change nothing
-            else
-              vv[v] = nv;
+            up[v] = uc[v];
+            vp[v] = vc[v];
+            dup[v] = duc[v];
+            dvp[v] = dvc[v];
+            uc[v] = ring[next][v];
           }
           prow = ringrow[j];
-          pin();
         }
         decode(Wn1, c + CH);
         Wn1 = Wn2;
@@ -666,13 +689,34 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
       // dropped, its v store lands in the spare slot).
       const int32_t full = len & ~(CH - 1);
       if (fold) {
+        // before rating 0 the pending update is a no-op on the ring's last
+        // slot (its current u, stored back unchanged)
         tcur = __uint_as_float(x64);
+        ep = 0.0f;
 #pragma unroll
-        for (int v = 0; v < NV; ++v) tcur = fmaf(-u[v], vv[v], tcur);
+        for (int v = 0; v < NV; ++v) {
+          tcur = fmaf(-u[v], vv[v], tcur);
+          up[v] = ring[D - 1][v];
+          vp[v] = vv[v];
+          dup[v] = 0.0f;
+          dvp[v] = 0.0f;
+          uc[v] = u[v];
+        }
+        prow = ringrow[D - 1];
         for (int32_t c = 0; c < full; c += CH) chunk_fold(std::false_type{}, c);
         if (full < len) chunk_fold(std::true_type{}, full);
-        if (full == len) st_row<NV, 0>(pnu, Ures, doff, prow);
-        lds_st<NV>(vv, waddr);
+        if (full == len) {
+          // the block's last rating: its update is still pending
+          const float ae = alpha * ep;
+#pragma unroll
+          for (int v = 0; v < NV; ++v) {
+            const float nu = up[v] + fmaf(ae, vp[v], dup[v]);
+            vp[v] = vp[v] + fmaf(ae, up[v], dvp[v]);
+            up[v] = nu;
+          }
+          st_row<NV, 0>(up, Ures, doff, prow);
+        }
+        lds_st<NV>(vp, waddr);
       } else {
         for (int32_t c = 0; c < full; c += CH) chunk(std::false_type{}, c);
         if (full < len) chunk(std::true_type{}, full);
