@@ -355,7 +355,8 @@ def main():
     if args.variant_steps > 0 and args.balanced_cuts == 0:
         # the same workload with nnz-balanced blocks (unequal block sizes, the
         # paper's suggested extension): a separate measurement, never `value`
-        rc, cc = bgmf.bgmf_balanced_cuts(w.n, w.m, w.p, w.rows, w.cols, 65536, 64)
+        cap = max(64, 2 * -(-w.m // w.p))  # narrow column-blocks that still cover m
+        rc, cc = bgmf.bgmf_balanced_cuts(w.n, w.m, w.p, w.rows, w.cols, 65536, cap)
         with bgmf.Model(w.n, w.m, w.k, w.p) as vm:
             vm.set_stream(stream.cuda_stream)
             vm.set_cuts(rc, cc)
@@ -373,8 +374,8 @@ def main():
         v_sweep = float(np.mean([x[0] for x in vs]))
         v_step = float(np.mean([x[0] + x[1] for x in vs]))
         variant = {
-            "blocks": "nnz-balanced cut points (bgmf_balanced_cuts, at most 64 columns per "
-                      "column-block)",
+            "blocks": f"nnz-balanced cut points (bgmf_balanced_cuts, at most {cap} columns "
+                      "per column-block)",
             "value": upd / (v_step / 1e3), "unit": "updates/s", "ms_per_step": v_step,
             "sweep_ms": v_sweep, "roofline_frac": upd * b_alg / (v_sweep / 1e3) / 1e9 / HBM_PEAK_GBS,
             "max_col_block": vchain[0], "max_row_block": vchain[1],
