@@ -19,19 +19,29 @@ __device__ __forceinline__ float dpp_mov(float x) {
   return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
 }
 
-// KP: padded k; L lanes per rating (4, 8 or 16); each lane covers the
-// float4 slices q = g, g + L, ... of the row.
+// Lanes per rating: from k = 32 up, each lane holds four float4 slices of
+// u_i and of v_j (KP/16 lanes per rating), which keeps the cross-lane levels
+// and the per-rating index work per wave step low; at k = 16 four lanes
+// hold one slice each.  Wave steps whose loads are in flight together: two
+// at four slices per lane, eight at one.
+template <int KP>
+constexpr int rmse_lanes() { return KP >= 32 ? KP / 16 : KP / 4; }
+template <int KP>
+constexpr int rmse_unroll() { return KP >= 32 ? 2 : 8; }
+
+// KP: padded k; L lanes per rating; each lane covers the float4 slices
+// q = g, g + L, ... of the row.
 template <int KP>
 __global__ void __launch_bounds__(256)
 k_rmse_partial(const uint2 *__restrict__ rec, const int64_t *__restrict__ wblock_ptr,
                const float *__restrict__ U, const float *__restrict__ V, Grid G, int32_t k,
                double *__restrict__ partials) {
   const int32_t p = G.p;
-  constexpr int L = KP >= 64 ? 16 : KP / 4;  // lanes per rating
+  constexpr int L = rmse_lanes<KP>();  // lanes per rating
   constexpr int RPS = 64 / L;                // ratings per wave step
   constexpr int Q = KP / 4;                  // float4 slices per padded row
   constexpr int QL = (Q + L - 1) / L;        // slices per lane
-  constexpr int UNR = 8;                     // wave steps whose loads are in flight together
+  constexpr int UNR = rmse_unroll<KP>();  // wave steps whose loads are in flight together
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int gl = lane % L, grp = lane / L;
   const int b = blockIdx.x / kRmseSplit;          // row-block
@@ -121,11 +131,11 @@ k_rmse_stratum(const uint2 *__restrict__ rec, int64_t rec_origin,
                const float *__restrict__ U, const float *__restrict__ V, Grid G, int32_t k,
                double *__restrict__ partials) {
   const int32_t p = G.p;
-  constexpr int L = KP >= 64 ? 16 : KP / 4;
+  constexpr int L = rmse_lanes<KP>();
   constexpr int RPS = 64 / L;
   constexpr int Q = KP / 4;
   constexpr int QL = (Q + L - 1) / L;
-  constexpr int UNR = 8;
+  constexpr int UNR = rmse_unroll<KP>();
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int gl = lane % L, grp = lane / L;
   const int b = blockIdx.x * kWavesPerGroup + wave;
@@ -195,7 +205,7 @@ __global__ void __launch_bounds__(256)
 k_rmse_coo(const int32_t *__restrict__ rows, const int32_t *__restrict__ cols,
            const float *__restrict__ vals, int64_t nnz, const float *__restrict__ U,
            const float *__restrict__ V, int32_t k, double *__restrict__ partials) {
-  constexpr int L = KP >= 64 ? 16 : KP / 4;
+  constexpr int L = rmse_lanes<KP>();
   constexpr int RPS = 64 / L;
   constexpr int Q = KP / 4;
   constexpr int QL = (Q + L - 1) / L;
@@ -255,11 +265,11 @@ k_rmse_lds(const uint2 *__restrict__ rec, const int64_t *__restrict__ wblock_ptr
            const float *__restrict__ U, const float *__restrict__ V, Grid G, int32_t k,
            double *__restrict__ partials) {
   const int32_t p = G.p;
-  constexpr int L = KP >= 64 ? 16 : KP / 4;
+  constexpr int L = rmse_lanes<KP>();
   constexpr int RPS = 64 / L;
   constexpr int Q = KP / 4;
   constexpr int QL = (Q + L - 1) / L;
-  constexpr int UNR = 8;
+  constexpr int UNR = rmse_unroll<KP>();
   extern __shared__ float4 us[];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int gl = lane % L, grp = lane / L;
