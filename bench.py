@@ -427,8 +427,11 @@ def main():
         "cpu_baseline": cpu,
         "balanced_blocks_variant": variant,
         "sweep_ms": sweep_avg,
+        "sweep_ms_median": float(np.median(sweep_ms)),
+        "sweep_ms_min": float(np.min(sweep_ms)),
         "sweep_updates_per_s": upd / (sweep_avg / 1e3),
         "rmse_pass_ms": float(np.mean(rmse_ms)),
+        "rmse_pass_ms_median": float(np.median(rmse_ms)),
         "load_bucket_s": t_load,
         "chain": {"max_col_block": chain[0], "max_row_block": chain[1],
                   "sum_stratum_max": chain[2], "nonempty_blocks": chain[3],

@@ -264,6 +264,11 @@ int bgmf_factor_ptrs(bgmf_t *h, float **U_dev, float **V_dev);
                                     wave be resident.  0: every hand-over goes
                                     through global memory.  Same arithmetic, so
                                     the results are bit-identical. */
+#define BGMF_OPT_TRACE 13        /* 1: each bgmf_epoch records a block trace
+                                    (bgmf_get_trace); the handle holds 16 p^2
+                                    bytes of device memory for it while on.
+                                    0 (default): off, and that memory is
+                                    freed.  The results do not change. */
 int bgmf_set_option(bgmf_t *h, int32_t option, int64_t value);
 int bgmf_get_option(const bgmf_t *h, int32_t option, int64_t *value);
 
@@ -271,6 +276,22 @@ int bgmf_get_option(const bgmf_t *h, int32_t option, int64_t *value);
  * events on the handle's stream around their kernels, in milliseconds
  * (NaN if not run yet).  Waits for the stream. */
 int bgmf_get_timing(bgmf_t *h, double *epoch_ms, double *rmse_ms);
+
+/* Block trace of the most recent bgmf_epoch (with BGMF_OPT_TRACE on), a
+ * tool for checking and analysing the stratum schedule of Section 1.1
+ * (Algorithm 1's inner loop): for block slot q = s*p + b (the block
+ * (b, (b+s) mod p) of stratum s),
+ *   begin[q] = device clock when the block starts, after its waits for the
+ *              previous holder of its column-block (a neighbour's progress
+ *              or, with one launch per stratum, the launch boundary);
+ *   end[q]   = device clock when the block hands its results on, before its
+ *              progress word moves.
+ * A block that no launch of the epoch visited (an empty stratum of a
+ * streamed epoch) has begin = end = 0.  Values are ticks of the device's
+ * constant-rate clock, *ticks_per_s per second.  begin and end are host
+ * arrays of p*p values each, owned by the caller.  Waits for the stream.
+ * BGMF_E_STATE if no epoch was traced since the option was set. */
+int bgmf_get_trace(bgmf_t *h, int64_t *begin, int64_t *end, int64_t *ticks_per_s);
 
 /* Serial-chain statistics of the loaded ratings, from the block sizes:
  *   out[0] = largest column-block total  (max_C sum_R nnz(R, C))

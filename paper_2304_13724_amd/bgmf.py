@@ -38,13 +38,14 @@ BGMF_OPT_RESIDENT_STRATA = 9
 BGMF_OPT_BLOCK_PASSES = 10
 BGMF_OPT_SINGLE_COLUMN = 11
 BGMF_OPT_LDS_HANDOVER = 12
+BGMF_OPT_TRACE = 13
 
 EXPORTED = (
     "bgmf_create", "bgmf_destroy", "bgmf_last_error", "bgmf_set_stream", "bgmf_set_factors",
     "bgmf_load_coo", "bgmf_epoch", "bgmf_rmse", "bgmf_get_factors", "bgmf_get_layout",
     "bgmf_sync", "bgmf_factor_ptrs", "bgmf_set_option", "bgmf_get_option", "bgmf_get_timing",
     "bgmf_chain_stats", "bgmf_rmse_coo", "bgmf_fit", "bgmf_set_cuts", "bgmf_get_cuts",
-    "bgmf_balanced_cuts",
+    "bgmf_balanced_cuts", "bgmf_get_trace",
 )
 
 
@@ -79,6 +80,7 @@ def _load() -> ctypes.CDLL:
         "bgmf_get_timing": ([vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)],
                             c_int),
         "bgmf_chain_stats": ([vp, vp], c_int),
+        "bgmf_get_trace": ([vp, vp, vp, ctypes.POINTER(I64)], c_int),
         "bgmf_rmse_coo": ([vp, vp, vp, vp, I64, ctypes.POINTER(ctypes.c_double)], c_int),
         "bgmf_fit": ([vp, F32, F32, I32, ctypes.c_double, ctypes.POINTER(I32), vp], c_int),
         "bgmf_set_cuts": ([vp, vp, vp], c_int),
@@ -202,6 +204,16 @@ def bgmf_chain_stats(h):
     return out
 
 
+def bgmf_get_trace(h, p: int):
+    """Block trace of the last epoch: (begin, end, ticks_per_s), begin and end
+    as [p, p] arrays indexed [s, b] (slot s*p + b)."""
+    begin = np.zeros(p * p, dtype=np.int64)
+    end = np.zeros(p * p, dtype=np.int64)
+    tps = ctypes.c_int64(0)
+    _check(h, _lib.bgmf_get_trace(h, _ptr(begin), _ptr(end), ctypes.byref(tps)))
+    return begin.reshape(p, p), end.reshape(p, p), int(tps.value)
+
+
 def bgmf_rmse_coo(h, rows, cols, vals) -> float:
     rows = np.ascontiguousarray(rows, dtype=np.int32)
     cols = np.ascontiguousarray(cols, dtype=np.int32)
@@ -318,6 +330,9 @@ class Model:
 
     def chain_stats(self):
         return bgmf_chain_stats(self.h)
+
+    def get_trace(self):
+        return bgmf_get_trace(self.h, self.p)
 
     def rmse_coo(self, rows, cols, vals) -> float:
         return bgmf_rmse_coo(self.h, rows, cols, vals)

@@ -51,6 +51,9 @@ struct bgmf {
   // options
   int64_t schedule = 0, wait_us = 10000000, xcd_remap = 1, v_staging = 0, passes = 1;
   int64_t single_col = 1, lds_handover = 1;
+  // block trace: [2 p p] clock values of the last epoch (see bgmf_get_trace)
+  int64_t *d_trace = nullptr;
+  bool trace_valid = false;
   // timing
   hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
   bool epoch_timed = false, rmse_timed = false;
@@ -319,6 +322,7 @@ void bgmf_destroy(bgmf_t *h) {
   hipFree(h->partials);
   hipFree(h->d_rmse);
   hipFree(h->d_cuts);
+  hipFree(h->d_trace);
   for (auto &ev : h->ev)
     if (ev) hipEventDestroy(ev);
   if (h->own_stream) hipStreamDestroy(h->own_stream);
@@ -653,6 +657,13 @@ int bgmf_epoch(bgmf_t *h, float alpha, float beta) {
   P.rowrep = h->rowrep;
   const SweepShape sh = sweep_shape(h);
   P.lds_ring = sh.lds ? h->lds_ring : 0;
+  if (h->d_trace) {
+    // blocks the epoch skips (empty strata of a streamed epoch) keep 0
+    h->trace_valid = false;
+    HIP_TRY(h, hipMemsetAsync(h->d_trace, 0, 2 * (size_t)h->p * h->p * sizeof(int64_t),
+                              h->stream));
+    P.trace = h->d_trace;
+  }
   HIP_TRY(h, hipEventRecord(h->ev[0], h->stream));
   if (h->ooc) {
     // resident strata, then the streamed chunks; each range is one
@@ -703,6 +714,7 @@ int bgmf_epoch(bgmf_t *h, float alpha, float beta) {
   HIP_TRY(h, hipEventRecord(h->ev[1], h->stream));
   h->epoch_timed = true;
   h->epochs_done += 1;
+  h->trace_valid = h->d_trace != nullptr;
   return BGMF_OK;
 }
 
@@ -1006,6 +1018,18 @@ int bgmf_set_option(bgmf_t *h, int32_t option, int64_t value) {
       return fail(h, BGMF_E_ARG, "BGMF_OPT_STREAM_CHUNKS is read-only");
     case BGMF_OPT_RESIDENT_STRATA:
       return fail(h, BGMF_E_ARG, "BGMF_OPT_RESIDENT_STRATA is read-only");
+    case BGMF_OPT_TRACE:
+      if (value != 0 && value != 1) return fail(h, BGMF_E_ARG, "trace must be 0 or 1");
+      if (value == 1 && !h->d_trace) {
+        HIP_TRY(h, hipStreamSynchronize(h->stream));
+        HIP_TRY(h, hipMalloc(&h->d_trace, 2 * (size_t)h->p * h->p * sizeof(int64_t)));
+      } else if (value == 0 && h->d_trace) {
+        HIP_TRY(h, hipStreamSynchronize(h->stream));
+        HIP_TRY(h, hipFree(h->d_trace));
+        h->d_trace = nullptr;
+      }
+      h->trace_valid = false;
+      return BGMF_OK;
     default:
       return fail(h, BGMF_E_ARG, "unknown option %d", option);
   }
@@ -1027,6 +1051,7 @@ int bgmf_get_option(const bgmf_t *h, int32_t option, int64_t *value) {
     case BGMF_OPT_BLOCK_PASSES: *value = h->passes; return BGMF_OK;
     case BGMF_OPT_SINGLE_COLUMN: *value = h->single_col; return BGMF_OK;
     case BGMF_OPT_LDS_HANDOVER: *value = h->lds_handover; return BGMF_OK;
+    case BGMF_OPT_TRACE: *value = h->d_trace ? 1 : 0; return BGMF_OK;
     case BGMF_OPT_PLACEMENT: {
       const SweepShape sh = sweep_shape(h);
       *value = (sh.lds ? 1 : 2) | (sh.persistent ? 4 : 0);
@@ -1055,6 +1080,26 @@ int bgmf_get_timing(bgmf_t *h, double *epoch_ms, double *rmse_ms) {
       *rmse_ms = ms;
     }
   }
+  return BGMF_OK;
+}
+
+int bgmf_get_trace(bgmf_t *h, int64_t *begin, int64_t *end, int64_t *ticks_per_s) {
+  if (!h) return BGMF_E_ARG;
+  if (!begin || !end || !ticks_per_s) return fail(h, BGMF_E_ARG, "bgmf_get_trace: null pointer");
+  if (!h->trace_valid)
+    return fail(h, BGMF_E_STATE, "bgmf_get_trace: no epoch traced since BGMF_OPT_TRACE was set");
+  int rc = sync_checked(h);
+  if (rc != BGMF_OK) return rc;
+  const size_t q = (size_t)h->p * h->p;
+  std::vector<int64_t> t(2 * q);
+  HIP_TRY(h, hipMemcpy(t.data(), h->d_trace, t.size() * sizeof(int64_t), hipMemcpyDeviceToHost));
+  for (size_t i = 0; i < q; ++i) {
+    begin[i] = t[2 * i];
+    end[i] = t[2 * i + 1];
+  }
+  int khz = 0;
+  HIP_TRY(h, hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, h->device));
+  *ticks_per_s = (int64_t)khz * 1000;
   return BGMF_OK;
 }
 

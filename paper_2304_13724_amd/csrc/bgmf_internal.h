@@ -78,6 +78,8 @@ struct SgdParams {
                              // block share a row
   int32_t lds_ring;          // LDS sweep, persistent launches: areas in the workgroup's
                              // hand-over ring (0: each wave its own area, global hand-over)
+  int64_t *trace;            // null, or [2 p p]: per block slot s*p + b, the clock when the
+                             // block starts and when it hands its results on
 };
 constexpr int kFlagStride = 16;  // int64 words per flag (one 128-byte line)
 constexpr int kWavesPerGroup = 4;

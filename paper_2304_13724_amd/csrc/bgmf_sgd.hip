@@ -224,6 +224,24 @@ __device__ __forceinline__ void publish_progress(int64_t *flag, int64_t value) {
   __hip_atomic_store(flag, value, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// Block trace (off unless the handle asks for it): lane 0 stores the
+// device's constant-rate clock with a vector store.  Slot 2q of the trace is
+// the time block q = s*p + b starts (after its waits), slot 2q + 1 the time
+// it hands its results on (before its progress word moves).
+__device__ __forceinline__ void trace_mark(int64_t *trace, int64_t slot, int lane) {
+  const int64_t t = (int64_t)__builtin_amdgcn_s_memrealtime();
+  if (lane == 0) trace[slot] = t;
+}
+
+// Ratings left in a block's last chunk, as a value the compiler cannot see
+// through: the per-step tests against it then stay inside that chunk instead
+// of being computed ahead for every block (and spilled) at its start.
+__device__ __forceinline__ int32_t tail_left(int32_t len, int32_t c) {
+  int32_t left = len - c;
+  asm volatile("" : "+s"(left));
+  return left;
+}
+
 // In-row sum (16 lanes) leaving the row's total in every lane of the row.
 __device__ __forceinline__ float row_sum(float x) {
 #pragma clang fp contract(off)
@@ -417,6 +435,7 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
         return;
       }
     }
+    if (P.trace) trace_mark(P.trace, 2 * ((int64_t)s * P.p + b), lane);
     const __amdgpu_buffer_rsrc_t Vres = __builtin_amdgcn_make_buffer_rsrc(
         P.V + c0 * k, (short)0, (int)((uint32_t)ncols * rowbytes), kBufWord3);
     if (stage) {
@@ -483,6 +502,7 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
       // of the plain order, so the results are the same bits.
       auto chunk = [&](auto tail_tag, int32_t c) {
         constexpr bool TAIL = decltype(tail_tag)::value;
+        const int32_t left = TAIL ? tail_left(len, c) : CH;
         // records c .. c+63 are decoded and those of chunk c+CH are in
         // flight; fetch the window two chunks ahead now
         const uint2 Wn2 = rp[c + 2 * CH + lane];
@@ -508,7 +528,7 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
           // consumed one step ago); this order is measurably faster than
           // the lane read first
           if constexpr (TAIL)
-            st_row<NV, 0>(pnu, Ures, doff + ((c + j - 1 < len) ? prow : kOff), 0);
+            st_row<NV, 0>(pnu, Ures, doff + ((j - 1 < left) ? prow : kOff), 0);
           else
             st_row<NV, 0>(pnu, Ures, doff, prow);
           pin();
@@ -596,6 +616,7 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
       float up[NV], vp[NV], dup[NV], dvp[NV], uc[NV];
       auto chunk_fold = [&](auto tail_tag, int32_t c) {
         constexpr bool TAIL = decltype(tail_tag)::value;
+        const int32_t left = TAIL ? tail_left(len, c) : CH;
         const uint2 Wn2 = rp[c + 2 * CH + lane];
 #pragma unroll
         for (int j = 0; j < CH; ++j) {
@@ -615,7 +636,7 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
 #pragma unroll
           for (int v = 0; v < NV; ++v) {
             if constexpr (TAIL)
-              vc[v] = (c + j - 1 < len) ? vp[v] + nvx[v] : vp[v];
+              vc[v] = (j - 1 < left) ? vp[v] + nvx[v] : vp[v];
             else
               vc[v] = vp[v] + nvx[v];
           }
@@ -663,7 +684,7 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
           pin();
           // rating t - 1's u (dropped past the block end)
           if constexpr (TAIL)
-            st_row<NV, 0>(nu, Ures, doff + ((c + j - 1 < len) ? prow : kOff), 0);
+            st_row<NV, 0>(nu, Ures, doff + ((j - 1 < left) ? prow : kOff), 0);
           else
             st_row<NV, 0>(nu, Ures, doff, prow);
           pin();
@@ -738,6 +759,7 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
           st_row<NV, kCoherent>(tmp[i], Vres, doff + (uint32_t)(cb + i) * rowbytes, 0);
       }
     }
+    if (P.trace) trace_mark(P.trace, 2 * ((int64_t)s * P.p + b) + 1, lane);
     // a launch of one stratum is ordered by the kernel boundary instead;
     // every lane publishes its own stores (all write the same value)
     if (P.s_end - P.s_begin > 1 && !to_lds)
@@ -850,6 +872,7 @@ __global__ void __launch_bounds__(256) k_sgd_gv(SgdParams P) {
         return;
       }
     }
+    if (P.trace) trace_mark(P.trace, 2 * ((int64_t)s * P.p + b), lane);
     if (len > 0) {
       const __amdgpu_buffer_rsrc_t Vres = __builtin_amdgcn_make_buffer_rsrc(
           P.V + c0 * k, (short)0, (int)((uint32_t)ncols * rowbytes), kBufWord3);
@@ -871,6 +894,7 @@ __global__ void __launch_bounds__(256) k_sgd_gv(SgdParams P) {
 
       auto chunk = [&](auto tail_tag, int32_t c) {
         constexpr bool TAIL = decltype(tail_tag)::value;
+        const int32_t left = TAIL ? tail_left(len, c) : CH;
         // window of chunk c + 2 CH (ratings c + CH .. c + CH + 63)
         const uint2 Wn2 = rp[c + CH + lane];
         uint32_t ccur = rl(wcol, CH);
@@ -907,7 +931,7 @@ __global__ void __launch_bounds__(256) k_sgd_gv(SgdParams P) {
           }
           lds_st<NV>(nv, ldsb, rbase + (uint32_t)j * slotbytes);
           if constexpr (TAIL) {
-            const bool real = c + j < len;
+            const bool real = j < left;
             st_row<NV, 0>(nu, Ures, doff + (real ? row : kOff), 0);
             st_row<NV, VPOL>(nv, Vres, doff + (real ? ccur : kOff), 0);
           } else {
@@ -934,6 +958,7 @@ __global__ void __launch_bounds__(256) k_sgd_gv(SgdParams P) {
       if (full < len) chunk(std::true_type{}, full);
       }
     }
+    if (P.trace) trace_mark(P.trace, 2 * ((int64_t)s * P.p + b) + 1, lane);
     if (P.s_end - P.s_begin > 1) publish_progress(P.flags + (int64_t)b * kFlagStride, g + 1);
   }
 }
