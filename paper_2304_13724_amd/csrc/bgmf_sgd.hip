@@ -234,8 +234,8 @@ __device__ __forceinline__ void trace_mark(int64_t *trace, int64_t slot, int lan
 }
 
 // Ratings left in a block's last chunk, as a value the compiler cannot see
-// through: the per-step tests against it then stay inside that chunk instead
-// of being computed ahead for every block (and spilled) at its start.
+// through: the per-step exit tests against it then stay inside that chunk
+// instead of being computed ahead for every block (and spilled) at its start.
 __device__ __forceinline__ int32_t tail_left(int32_t len, int32_t c) {
   int32_t left = len - c;
   asm volatile("" : "+s"(left));
@@ -485,10 +485,10 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
         pnv[v] = vv[v];
       }
 
-      // One chunk of CH ratings, fully unrolled.  In a full chunk every
-      // step is a real rating and U is addressed with the row as a scalar
-      // offset; the last, partial chunk of a block sends the U store of each
-      // step past the end to an out-of-range vector offset (dropped).
+      // One chunk of CH ratings, fully unrolled, U addressed with the row as
+      // a scalar offset; the last, partial chunk of a block leaves the loop
+      // after the block's last rating (a uniform branch per step), so no
+      // step runs on padding.
       //
       // A step is one dependent chain: partial products, six cross-lane
       // levels, the lane read of e, the update, and the choice of the next
@@ -527,10 +527,7 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
           // previous one, whose ring slot is free again (its value was
           // consumed one step ago); this order is measurably faster than
           // the lane read first
-          if constexpr (TAIL)
-            st_row<NV, 0>(pnu, Ures, doff + ((j - 1 < left) ? prow : kOff), 0);
-          else
-            st_row<NV, 0>(pnu, Ures, doff, prow);
+          st_row<NV, 0>(pnu, Ures, doff, prow);
           pin();
           ringrow[slot] = rl(wrow, slot + D - (j == 0 ? CH : 0));
           pin();
@@ -590,6 +587,9 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
           ncol = col2;
           naddr = naddr2;
           pin();
+          if constexpr (TAIL) {
+            if (j + 1 >= left) break;
+          }
         }
         decode(Wn1, c + CH);
         Wn1 = Wn2;
@@ -632,13 +632,10 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
           t = t + dpp_mov<0xB1>(t);  // quad_perm [1,0,3,2]
           pin();
           ringrow[slot] = rl(wrow, slot + D - (j == 0 ? CH : 0));
-          // v of rating t (rating t - 1's result; unchanged past the block end)
+          // v of rating t (rating t - 1's result)
 #pragma unroll
           for (int v = 0; v < NV; ++v) {
-            if constexpr (TAIL)
-              vc[v] = (j - 1 < left) ? vp[v] + nvx[v] : vp[v];
-            else
-              vc[v] = vp[v] + nvx[v];
+            vc[v] = vp[v] + nvx[v];
           }
           pin();
           t = t + dpp_mov<0x4E>(t);  // quad_perm [2,3,0,1]
@@ -682,11 +679,8 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
           pin();
           const float e = __uint_as_float(rl(__float_as_uint(t), 63));
           pin();
-          // rating t - 1's u (dropped past the block end)
-          if constexpr (TAIL)
-            st_row<NV, 0>(nu, Ures, doff + ((j - 1 < left) ? prow : kOff), 0);
-          else
-            st_row<NV, 0>(nu, Ures, doff, prow);
+          // rating t - 1's u
+          st_row<NV, 0>(nu, Ures, doff, prow);
           pin();
           tcur = fmaf(-e, B, A);
           pin();
@@ -700,14 +694,16 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
             uc[v] = ring[next][v];
           }
           prow = ringrow[j];
+          if constexpr (TAIL) {
+            if (j + 1 >= left) break;
+          }
         }
         decode(Wn1, c + CH);
         Wn1 = Wn2;
       };
 
-      // The results of the block's last step are still pending; after a
-      // partial chunk they belong to a step past the end (its u store is
-      // dropped, its v store lands in the spare slot).
+      // After the last chunk (a partial one stops right after the block's
+      // last rating) that rating's results are still pending.
       const int32_t full = len & ~(CH - 1);
       if (fold) {
         // before rating 0 the pending update is a no-op on the ring's last
@@ -726,7 +722,7 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
         prow = ringrow[D - 1];
         for (int32_t c = 0; c < full; c += CH) chunk_fold(std::false_type{}, c);
         if (full < len) chunk_fold(std::true_type{}, full);
-        if (full == len) {
+        {
           // the block's last rating: its update is still pending
           const float ae = alpha * ep;
 #pragma unroll
@@ -741,7 +737,7 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
       } else {
         for (int32_t c = 0; c < full; c += CH) chunk(std::false_type{}, c);
         if (full < len) chunk(std::true_type{}, full);
-        if (full == len) st_row<NV, 0>(pnu, Ures, doff, prow);
+        st_row<NV, 0>(pnu, Ures, doff, prow);
         lds_st<NV>(pnv, pwaddr);
       }
       }
@@ -930,14 +926,8 @@ __global__ void __launch_bounds__(256) k_sgd_gv(SgdParams P) {
             nv[v] = vv[v] + fmaf(ae, u[v], nab * vv[v]);
           }
           lds_st<NV>(nv, ldsb, rbase + (uint32_t)j * slotbytes);
-          if constexpr (TAIL) {
-            const bool real = j < left;
-            st_row<NV, 0>(nu, Ures, doff + (real ? row : kOff), 0);
-            st_row<NV, VPOL>(nv, Vres, doff + (real ? ccur : kOff), 0);
-          } else {
-            st_row<NV, 0>(nu, Ures, doff, row);
-            st_row<NV, VPOL>(nv, Vres, doff, ccur);
-          }
+          st_row<NV, 0>(nu, Ures, doff, row);
+          st_row<NV, VPOL>(nv, Vres, doff, ccur);
 #pragma unroll
           for (int v = 0; v < NV; ++v) {
             uprev[v] = nu[v];
@@ -949,6 +939,9 @@ __global__ void __launch_bounds__(256) k_sgd_gv(SgdParams P) {
           ringrow[j] = rl(wrow, 2 * CH + j);
           ld_row<NV, 0>(ring[j], Ures, doff, ringrow[j]);
           ld_row<NV, VPOL>(vring[j], Vres, doff, rl(wcol, 2 * CH + j));
+          if constexpr (TAIL) {
+            if (j + 1 >= left) break;  // the block's last rating is done
+          }
         }
         decode(Wn1, c + CH);
         Wn1 = Wn2;
