@@ -81,6 +81,20 @@ namespace {
 
 thread_local std::string g_create_error;
 
+// Zeroes the block trace with a kernel rather than a memset, so that an
+// epoch stays a sequence of kernel launches.
+__global__ void k_clear_i64(int64_t *x, int64_t count) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count;
+       i += (int64_t)gridDim.x * blockDim.x)
+    x[i] = 0;
+}
+
+hipError_t clear_trace(int64_t *trace, int64_t count, hipStream_t stream) {
+  const int64_t blocks = std::max<int64_t>(1, std::min<int64_t>((count + 255) / 256, 4096));
+  hipLaunchKernelGGL(k_clear_i64, dim3((unsigned)blocks), dim3(256), 0, stream, trace, count);
+  return hipGetLastError();
+}
+
 int fail(bgmf_t *h, int code, const char *fmt, ...) {
   char buf[512];
   va_list ap;
@@ -660,8 +674,7 @@ int bgmf_epoch(bgmf_t *h, float alpha, float beta) {
   if (h->d_trace) {
     // blocks the epoch skips (empty strata of a streamed epoch) keep 0
     h->trace_valid = false;
-    HIP_TRY(h, hipMemsetAsync(h->d_trace, 0, 2 * (size_t)h->p * h->p * sizeof(int64_t),
-                              h->stream));
+    HIP_TRY(h, clear_trace(h->d_trace, 2 * (int64_t)h->p * h->p, h->stream));
     P.trace = h->d_trace;
   }
   HIP_TRY(h, hipEventRecord(h->ev[0], h->stream));
