@@ -109,6 +109,8 @@ def summary(begin: np.ndarray, end: np.ndarray, ticks_per_s: int) -> dict:
     column hand-over latencies, in microseconds."""
     us = 1e6 / ticks_per_s
     seen = _traced(begin, end)
+    if not seen.any():
+        return {"span_us": 0.0, "blocks": 0}
     span = (end[seen].max() - begin[seen].min()) * us
     out = {"span_us": float(span), "blocks": int(seen.sum())}
     if seen.all():

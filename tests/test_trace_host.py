@@ -95,3 +95,12 @@ def test_handover_gaps_are_the_latency():
     out = T.summary(b, e, 100_000_000)
     assert out["handover_us_median"] == pytest.approx(0.07)
     assert out["critical_busy_us"] + out["critical_wait_us"] <= out["span_us"] + 1e-9
+
+
+def test_degenerate_traces():
+    z = np.zeros((3, 3), np.int64)
+    assert T.violations(z, z) == [] and T.summary(z, z, 100_000_000) == {"span_us": 0.0, "blocks": 0}
+    b, e = _simulate(1, 0)  # p = 1: one block, no hand-overs
+    assert T.violations(b, e) == [] and T.handover_gaps(b, e).size == 0
+    path, busy, wait = T.critical_path(b, e)
+    assert path == [(0, 0)] and busy == e[0, 0] - b[0, 0] and wait == 0
