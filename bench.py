@@ -49,6 +49,9 @@ def parse():
                     help="BGMF_OPT_SINGLE_COLUMN: 1 (default) lets blocks of a one-column "
                          "column-block keep v in registers, 0 sends them through the "
                          "general step")
+    ap.add_argument("--trace", type=int, default=0, choices=(0, 1),
+                    help="after the timed region, run one more epoch with the block trace on and "
+                         "report its schedule check and critical path (trace_summary)")
     ap.add_argument("--model", type=int, default=1, choices=(0, 1),
                     help="after the timed region, time one dependent chain of general steps "
                          "(t_dep, for the chain bound N / (sum of stratum maxima x t_dep)) "
@@ -381,6 +384,19 @@ def main():
             "max_col_block": vchain[0], "max_row_block": vchain[1],
         }
         log(f"balanced blocks: sweep {v_sweep:.2f} ms, step {v_step:.2f} ms")
+    trace_summary = None
+    if args.trace:
+        # one more epoch, traced (never part of the timed region)
+        from paper_2304_13724_amd import trace as T
+        mdl.set_option(bgmf.BGMF_OPT_TRACE, 1)
+        mdl.epoch(w.alpha, w.beta)
+        tb, te, tps = mdl.get_trace()
+        mdl.set_option(bgmf.BGMF_OPT_TRACE, 0)
+        per_stratum = not (mdl.get_option(bgmf.BGMF_OPT_PLACEMENT) & 4)
+        trace_summary = T.summary(tb, te, tps)
+        trace_summary["violations"] = len(T.violations(tb, te, per_stratum=per_stratum))
+        trace_summary["epoch_ms_traced"] = mdl.timing()[0]
+        log(f"trace: {trace_summary}")
     t_dep, copy_gbs = chain_model(stream) if args.model else (None, None)
     cpu = None
     if args.cpu_seconds > 0:
@@ -443,6 +459,7 @@ def main():
         "frac_vs_copy": achieved / copy_gbs if copy_gbs else None,
         "rmse_last": rmses[-1],
         "wall_s": wall,
+        "trace_summary": trace_summary,
     }
     mdl.close()
     print(json.dumps(out), flush=True)
