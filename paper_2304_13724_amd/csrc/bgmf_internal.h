@@ -80,6 +80,9 @@ struct SgdParams {
                              // hand-over ring (0: each wave its own area, global hand-over)
   int64_t *trace;            // null, or [2 p p]: per block slot s*p + b, the clock when the
                              // block starts and when it hands its results on
+  int32_t wpg;               // waves per workgroup (set by launch_sgd; a kernel argument
+                             // arrives with the others, blockDim from the dispatch packet
+                             // would cost a memory round trip at every launch)
 };
 constexpr int kFlagStride = 16;  // int64 words per flag (one 128-byte line)
 constexpr int kWavesPerGroup = 4;

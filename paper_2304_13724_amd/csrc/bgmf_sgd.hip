@@ -296,7 +296,7 @@ __device__ __forceinline__ int row_block_of_wave(const SgdParams &P, int wave) {
     const int G = gridDim.x;
     grp = (blockIdx.x & 7) * (G >> 3) + (blockIdx.x >> 3);
   }
-  return grp * (int)(blockDim.x >> 6) + wave;
+  return grp * P.wpg + wave;
 }
 
 // Error term: every lane adds x/KPL to its partial products, so the lane
@@ -311,7 +311,7 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
   static_assert((CH & (CH - 1)) == 0 && CH <= 32,
                 "full chunks are counted with a mask; lanes j + D stay in the 64-record window");
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
-  const int wpg = (int)(blockDim.x >> 6);
+  const int wpg = P.wpg;
   const int b = row_block_of_wave(P, wave);
   const L ln(P.k);
   const int lane = ln.lane;
@@ -1011,6 +1011,7 @@ hipError_t launch_sgd(const SgdParams &P, int kp, int vmode, int waves_per_group
   const unsigned groups = (unsigned)((P.p + waves_per_group - 1) / waves_per_group);
   const unsigned threads = 64u * (unsigned)waves_per_group;
   SgdParams args = P;
+  args.wpg = waves_per_group;
   if (args.xcd_remap && (groups % 8) != 0) args.xcd_remap = 0;
   void *kargs[] = {&args};
   if (cooperative)
