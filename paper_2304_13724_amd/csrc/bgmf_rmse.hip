@@ -1,7 +1,9 @@
 // Whole-matrix RMSE over the loaded ratings (Algorithm 1's termination
 // test): sqrt((1/nnz) sum (x - u_i.v_j)^2), dot products in fp32, squares
-// summed in fp64.  Reads the wave-major records: workgroup b covers
-// row-block b, its wave w the blocks s = w, w+4, ...; a group of lanes
+// summed in fp64.  Reads the wave-major records.  With the row-block's U
+// rows in LDS (k_rmse_lds) a workgroup covers one row-block; otherwise
+// (k_rmse_partial) a workgroup covers one row-block and a group of
+// column-blocks, its wave w every fourth of them from w.  A group of lanes
 // shares one rating and loads 16-byte slices of u_i and v_j.  Per-wave sums
 // are combined in a fixed order by a second kernel, so the result does not
 // depend on scheduling.
@@ -12,7 +14,11 @@
 namespace bgmfk {
 namespace {
 
-constexpr int kRmseSplit = 4;  // workgroups per row-block (each takes a quarter of its strata)
+// Column-blocks per workgroup of k_rmse_partial.  Workgroups are numbered
+// group-major (all row-blocks of column-blocks 0..63, then 64..127, ...), so
+// the workgroups resident at one time read the V rows of about 64
+// column-blocks, which stay in the caches, instead of all of V.
+constexpr int kRmseColGroup = 64;
 
 template <int CTRL>
 __device__ __forceinline__ float dpp_mov(float x) {
@@ -44,13 +50,15 @@ k_rmse_partial(const uint2 *__restrict__ rec, const int64_t *__restrict__ wblock
   constexpr int UNR = rmse_unroll<KP>();  // wave steps whose loads are in flight together
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int gl = lane % L, grp = lane / L;
-  const int b = blockIdx.x / kRmseSplit;          // row-block
-  const int w0 = (blockIdx.x % kRmseSplit) * kWavesPerGroup + wave;  // first stratum
+  const int b = blockIdx.x % p;    // row-block
+  const int cg = blockIdx.x / p;   // group of column-blocks
+  const int c_end = min(p, (cg + 1) * kRmseColGroup);
   const float *Ub = U + G.row_start(b) * k;
   const uint32_t rmax = (uint32_t)(G.row_start(b + 1) - G.row_start(b)) - 1u;
   const int kq = k / 4;
   double acc = 0.0;
-  for (int s = w0; s < p; s += kWavesPerGroup * kRmseSplit) {
+  for (int c = cg * kRmseColGroup + wave; c < c_end; c += kWavesPerGroup) {
+    const int s = (c - b + p) % p;  // block (b, c) is in stratum s
     const int64_t beg = wblock_ptr[(int64_t)b * p + s];
     const int64_t end = wblock_ptr[(int64_t)b * p + s + 1];
     if (beg == end) continue;
@@ -397,7 +405,8 @@ k_rmse_final(const double *__restrict__ partials, int64_t count, int64_t nnz, do
 }  // namespace
 
 size_t rmse_partials_count(int32_t p) {
-  return (size_t)p * (size_t)std::max(kRmseSplit * kWavesPerGroup, kLdsWaves);
+  const int64_t groups = ((int64_t)p + kRmseColGroup - 1) / kRmseColGroup;
+  return (size_t)p * (size_t)std::max<int64_t>(groups * kWavesPerGroup, kLdsWaves);
 }
 
 namespace {
@@ -422,9 +431,10 @@ hipError_t launch_rmse_kp(const uint2 *rec, const int64_t *wblock_ptr, const flo
                        wblock_ptr, U, V, G, k, partials);
     *count = (int64_t)p * kLdsWaves;
   } else {
-    hipLaunchKernelGGL(k_rmse_partial<KP>, dim3((unsigned)(p * kRmseSplit)), dim3(256), 0, stream,
+    const int64_t groups = (int64_t)p * ((p + kRmseColGroup - 1) / kRmseColGroup);
+    hipLaunchKernelGGL(k_rmse_partial<KP>, dim3((unsigned)groups), dim3(256), 0, stream,
                        rec, wblock_ptr, U, V, G, k, partials);
-    *count = (int64_t)p * kRmseSplit * kWavesPerGroup;
+    *count = groups * kWavesPerGroup;
   }
   return hipGetLastError();
 }
