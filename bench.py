@@ -272,9 +272,9 @@ def main():
                           "(sharding across GPUs is designed but not implemented)"}))
         sys.exit(2)
     import numpy as np
-    import torch
 
-    from paper_2304_13724_amd import bgmf
+    from paper_2304_13724_amd import bgmf  # before torch: one HIP runtime in the process
+    import torch
     from workloads import make_config
 
     torch.cuda.set_device(0)

@@ -56,10 +56,11 @@ extern "C" {
 #define BGMF_E_RANGE      -3  /* a rating index outside [0,n) x [0,m) */
 #define BGMF_E_NONFINITE  -4  /* a rating value that is NaN or infinite */
 #define BGMF_E_NOMEM      -5  /* device or host allocation failed */
-#define BGMF_E_UNSUPPORTED -6 /* shape the kernels do not handle */
+#define BGMF_E_BUDGET     -6  /* the ratings budget, a bound workspace or a bound host
+                                 arena is too small for the loaded ratings */
 #define BGMF_E_HIP        -7  /* a HIP runtime call failed */
-#define BGMF_E_TIMEOUT    -8  /* a device-side wait between strata exceeded its limit */
-#define BGMF_E_BUDGET     -9  /* the ratings budget cannot hold two strata */
+#define BGMF_E_UNSUPPORTED -8 /* shape the kernels do not handle */
+#define BGMF_E_TIMEOUT    -9  /* a device-side wait between strata exceeded its limit */
 
 typedef struct bgmf bgmf_t; /* opaque handle */
 
@@ -84,6 +85,55 @@ const char *bgmf_last_error(const bgmf_t *h);
  * example PyTorch's current stream).  NULL selects the handle's own stream.
  * The caller keeps ownership; the stream must outlive its use by h. */
 int bgmf_set_stream(bgmf_t *h, void *hip_stream);
+
+/* Memory a caller provides for a handle (bgmf_bind), for nnz ratings:
+ *   *factor_bytes    = bytes of U (n x k) plus V (m x k), fp32;
+ *   *incore_ws_bytes = a workspace that keeps every rating on the device:
+ *                      the block tables, 8-byte records (+256 of padding),
+ *                      perm, and the one-pass bucketing's temporaries (the
+ *                      COO arrays and the radix sort's scratch), about
+ *                      48 bytes per rating;
+ *   *min_ws_bytes    = a lower bound below which no load of nnz ratings can
+ *                      stream (the block tables, the bucketing of an average
+ *                      block and a ring of two average strata); the real
+ *                      need depends on the largest block and stratum, which
+ *                      bgmf_load_coo checks (BGMF_E_BUDGET);
+ *   *pinned_bytes    = a pinned host arena for streamed ratings (records and
+ *                      perm, 12 bytes per rating).
+ * Any output may be NULL.  The sizes follow the Problem of Section 1 (U,
+ * V) and Eq. 4 (the p x p block tables). */
+int bgmf_query_sizes(const bgmf_t *h, int64_t nnz, size_t *factor_bytes, size_t *min_ws_bytes,
+                     size_t *incore_ws_bytes, size_t *pinned_bytes);
+
+/* Bind caller-owned memory (for example PyTorch tensors) to the handle,
+ * before any ratings are loaded (else BGMF_E_STATE):
+ *   U_dev, V_dev  device memory of n x k and m x k fp32, row-major; from
+ *                 now on they ARE the factors (Algorithm 1's inputs and
+ *                 outputs): the handle's own U and V are freed, whatever
+ *                 the buffers hold counts as set factors, and
+ *                 bgmf_set_factors / bgmf_get_factors copy into / out of
+ *                 them;
+ *   ws_dev, ws_bytes  device workspace for the block tables and the
+ *                 ratings.  bgmf_load_coo keeps every rating on the device
+ *                 when ws_bytes >= incore_ws_bytes (bgmf_query_sizes) and
+ *                 BGMF_OPT_RATINGS_BUDGET allows it; otherwise the ratings
+ *                 stream, with ws_bytes minus the tables (or the budget
+ *                 option, if smaller) as their device budget;
+ *   pinned_host, pinned_bytes  pinned host memory (hipHostMalloc, or a
+ *                 PyTorch pin_memory tensor) for streamed ratings; NULL if
+ *                 the ratings will not stream;
+ *   hip_stream    as bgmf_set_stream (NULL: the handle's own stream).
+ * Every pointer must start on a 256-byte boundary; U, V and the workspace
+ * must be device memory of the handle's device (BGMF_E_ARG otherwise).  A
+ * workspace smaller than the tables -> BGMF_E_BUDGET.  The caller keeps
+ * ownership; the buffers must outlive their use by the handle and must not
+ * be used by the caller while the handle's work on them is in flight.  After
+ * binding, bgmf_load_coo, bgmf_epoch and bgmf_rmse allocate no memory
+ * (BGMF_OPT_ALLOC_COUNT does not move); the handle still allocates its
+ * small fixed tables at bgmf_create, the block trace when BGMF_OPT_TRACE is
+ * set, and bgmf_rmse_coo's temporaries. */
+int bgmf_bind(bgmf_t *h, float *U_dev, float *V_dev, void *ws_dev, size_t ws_bytes,
+              void *pinned_host, size_t pinned_bytes, void *hip_stream);
 
 /* Copy initial factors from host memory: U is n x k, V is m x k, row-major
  * fp32 (u_i = U[i*k .. i*k+k)).  Algorithm 1 starts from random factors;
@@ -163,8 +213,9 @@ int bgmf_rmse_coo(bgmf_t *h, const int32_t *rows, const int32_t *cols, const flo
 int bgmf_fit(bgmf_t *h, float alpha, float beta, int32_t max_epochs, double delta,
              int32_t *epochs_run, double *rmse_history);
 
-/* Copy the current factors to host memory (row-major n x k and m x k).
- * Either pointer may be NULL to skip it.  Waits for the stream. */
+/* Copy the current factors to host memory (row-major n x k and m x k):
+ * the U and V that Algorithm 1 returns.  Either pointer may be NULL to
+ * skip it.  Waits for the stream. */
 int bgmf_get_factors(bgmf_t *h, float *U, float *V);
 
 /* Bucketing result, for bit-exact checks:
@@ -179,8 +230,9 @@ int bgmf_get_layout(bgmf_t *h, int64_t *block_ptr, int32_t *perm);
  * failure of earlier asynchronous calls. */
 int bgmf_sync(bgmf_t *h);
 
-/* Device pointers of U (n x k) and V (m x k), row-major fp32, owned by the
- * handle and valid until bgmf_destroy.  Either output may be NULL. */
+/* Device pointers of U (n x k) and V (m x k), row-major fp32: the handle's
+ * own (valid until bgmf_destroy) or the caller's bound ones.  Either output
+ * may be NULL. */
 int bgmf_factor_ptrs(bgmf_t *h, float **U_dev, float **V_dev);
 
 /* Options (bgmf_set_option / bgmf_get_option). */
@@ -196,12 +248,17 @@ int bgmf_factor_ptrs(bgmf_t *h, float **U_dev, float **V_dev);
                                     (default 10,000,000) */
 #define BGMF_OPT_XCD_REMAP     3 /* 1 (default): place neighbouring row-blocks on
                                     the same XCD; 0: plain workgroup order */
-#define BGMF_OPT_RATINGS_BUDGET 4 /* device bytes the bucketed ratings may occupy
-                                    during epochs; 0 (default) = no limit.  Takes
-                                    effect at the next bgmf_load_coo.  If the
-                                    ratings (8 bytes each, plus 256 records of
-                                    padding) do not fit, they are kept in pinned
-                                    host memory in stratum order.  The budget is
+#define BGMF_OPT_RATINGS_BUDGET 4 /* device bytes the ratings may occupy, at load
+                                    and during epochs; 0 (default) = no limit.
+                                    Takes effect at the next bgmf_load_coo.  If
+                                    the one-pass bucketing (about 48 bytes per
+                                    rating, see bgmf_query_sizes) does not fit,
+                                    the ratings are kept in pinned host memory in
+                                    stratum order, bucketed group by group (each
+                                    group of whole blocks gathered from the input,
+                                    sorted on the device within the budget, and
+                                    copied out; the largest block must fit, else
+                                    BGMF_E_BUDGET).  The budget is
                                     then split into a ring of 3 (else 2) device
                                     slots and a resident region: the first strata
                                     of the epoch stay resident (copied once, at
@@ -269,6 +326,20 @@ int bgmf_factor_ptrs(bgmf_t *h, float **U_dev, float **V_dev);
                                     bytes of device memory for it while on.
                                     0 (default): off, and that memory is
                                     freed.  The results do not change. */
+#define BGMF_OPT_ALLOC_COUNT 14  /* read-only: device and pinned host allocations
+                                    the handle has made since bgmf_create */
+#define BGMF_OPT_LOAD_PEAK 15    /* read-only: device bytes the last bgmf_load_coo
+                                    used for ratings at its peak (records, perm,
+                                    bucketing temporaries, stream slots and
+                                    resident strata; block tables not counted);
+                                    within the ratings budget when one is set, or
+                                    within the bytes needed to bucket the largest
+                                    block if those are more (a handle that owns
+                                    its memory; a bound one stays within its
+                                    workspace or fails with BGMF_E_BUDGET) */
+#define BGMF_OPT_LOAD_GROUPS 16  /* read-only: groups of blocks the last streamed
+                                    bgmf_load_coo gathered and sorted one at a
+                                    time (0 for an in-core load) */
 int bgmf_set_option(bgmf_t *h, int32_t option, int64_t value);
 int bgmf_get_option(const bgmf_t *h, int32_t option, int64_t *value);
 

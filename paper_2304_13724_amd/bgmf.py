@@ -21,10 +21,10 @@ BGMF_E_STATE = -2
 BGMF_E_RANGE = -3
 BGMF_E_NONFINITE = -4
 BGMF_E_NOMEM = -5
-BGMF_E_UNSUPPORTED = -6
+BGMF_E_BUDGET = -6
 BGMF_E_HIP = -7
-BGMF_E_TIMEOUT = -8
-BGMF_E_BUDGET = -9
+BGMF_E_UNSUPPORTED = -8
+BGMF_E_TIMEOUT = -9
 
 BGMF_OPT_SCHEDULE = 1
 BGMF_OPT_WAIT_LIMIT_US = 2
@@ -39,13 +39,16 @@ BGMF_OPT_BLOCK_PASSES = 10
 BGMF_OPT_SINGLE_COLUMN = 11
 BGMF_OPT_LDS_HANDOVER = 12
 BGMF_OPT_TRACE = 13
+BGMF_OPT_ALLOC_COUNT = 14
+BGMF_OPT_LOAD_PEAK = 15
+BGMF_OPT_LOAD_GROUPS = 16
 
 EXPORTED = (
     "bgmf_create", "bgmf_destroy", "bgmf_last_error", "bgmf_set_stream", "bgmf_set_factors",
     "bgmf_load_coo", "bgmf_epoch", "bgmf_rmse", "bgmf_get_factors", "bgmf_get_layout",
     "bgmf_sync", "bgmf_factor_ptrs", "bgmf_set_option", "bgmf_get_option", "bgmf_get_timing",
     "bgmf_chain_stats", "bgmf_rmse_coo", "bgmf_fit", "bgmf_set_cuts", "bgmf_get_cuts",
-    "bgmf_balanced_cuts", "bgmf_get_trace",
+    "bgmf_balanced_cuts", "bgmf_get_trace", "bgmf_query_sizes", "bgmf_bind",
 )
 
 
@@ -86,6 +89,10 @@ def _load() -> ctypes.CDLL:
         "bgmf_set_cuts": ([vp, vp, vp], c_int),
         "bgmf_get_cuts": ([vp, vp, vp], c_int),
         "bgmf_balanced_cuts": ([I64, I64, I32, vp, vp, I64, I64, I64, vp, vp], c_int),
+        "bgmf_query_sizes": ([vp, I64, ctypes.POINTER(ctypes.c_size_t),
+                              ctypes.POINTER(ctypes.c_size_t), ctypes.POINTER(ctypes.c_size_t),
+                              ctypes.POINTER(ctypes.c_size_t)], c_int),
+        "bgmf_bind": ([vp, vp, vp, vp, ctypes.c_size_t, vp, ctypes.c_size_t, vp], c_int),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -131,6 +138,24 @@ def bgmf_set_stream(h, stream) -> None:
     """``stream``: an integer hipStream_t (e.g. torch.cuda.current_stream().cuda_stream)
     or None for the handle's own stream."""
     _check(h, _lib.bgmf_set_stream(h, ctypes.c_void_p(int(stream)) if stream else None))
+
+
+def bgmf_query_sizes(h, nnz: int):
+    """Returns dict(factor_bytes, min_ws_bytes, incore_ws_bytes, pinned_bytes)."""
+    out = [ctypes.c_size_t(0) for _ in range(4)]
+    _check(h, _lib.bgmf_query_sizes(h, int(nnz), *[ctypes.byref(o) for o in out]))
+    keys = ("factor_bytes", "min_ws_bytes", "incore_ws_bytes", "pinned_bytes")
+    return {k: int(o.value) for k, o in zip(keys, out)}
+
+
+def bgmf_bind(h, U_dev: int, V_dev: int, ws_dev: int, ws_bytes: int, pinned_host: int,
+              pinned_bytes: int, stream) -> None:
+    """Addresses as integers (for example ``tensor.data_ptr()``), ``pinned_host``
+    0 for none, ``stream`` an integer hipStream_t or None."""
+    def vp(x):
+        return ctypes.c_void_p(int(x)) if x else None
+    _check(h, _lib.bgmf_bind(h, vp(U_dev), vp(V_dev), vp(ws_dev), int(ws_bytes),
+                             vp(pinned_host), int(pinned_bytes), vp(stream)))
 
 
 def bgmf_set_factors(h, U: np.ndarray, V: np.ndarray) -> None:
@@ -299,6 +324,13 @@ class Model:
 
     def set_factors(self, U, V):
         bgmf_set_factors(self.h, U, V)
+
+    def query_sizes(self, nnz: int):
+        return bgmf_query_sizes(self.h, nnz)
+
+    def bind(self, U_dev: int, V_dev: int, ws_dev: int, ws_bytes: int, pinned_host: int = 0,
+             pinned_bytes: int = 0, stream=None):
+        bgmf_bind(self.h, U_dev, V_dev, ws_dev, ws_bytes, pinned_host, pinned_bytes, stream)
 
     def load_coo(self, rows, cols, vals):
         bgmf_load_coo(self.h, rows, cols, vals)

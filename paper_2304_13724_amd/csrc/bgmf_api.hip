@@ -13,73 +13,80 @@
 #include <vector>
 
 #include "../../include/bgmf.h"
-#include "bgmf_internal.h"
+#include "bgmf_handle.h"
 
 using namespace bgmfk;
-
-struct bgmf {
-  int64_t n = 0, m = 0;
-  int32_t k = 0, p = 0, kp = 0;
-  int device = 0;
-  int cus = 0;
-  hipStream_t own_stream = nullptr;
-  hipStream_t stream = nullptr;
-  float *U = nullptr, *V = nullptr;
-  // ratings layout
-  int64_t nnz = 0;
-  int64_t *block_ptr = nullptr, *wblock_ptr = nullptr;
-  uint8_t *rowrep = nullptr;  // [p*p] per block slot: a row repeats in consecutive ratings
-  int32_t *perm = nullptr;
-  uint2 *rec = nullptr;
-  int64_t *flags = nullptr;
-  int32_t *err = nullptr;
-  double *partials = nullptr, *d_rmse = nullptr;
-  int64_t epochs_done = 0;
-  bool factors_set = false, loaded = false;
-  // block cut points (host copies and device tables, p + 1 each)
-  std::vector<int64_t> rcut, ccut;
-  int64_t *d_cuts = nullptr;  // rcut then ccut
-  int64_t rows_max = 0;
-  // launch shapes: V slice staged in LDS (when it fits) and V in global memory
-  int cols_max = 0;
-  size_t lds_limit = 0;
-  bool lds_fits = false;
-  int wpg_lds = 1, wpg_gv = kWavesPerGroup;
-  int lds_ring = 0;  // areas of the LDS hand-over ring (0: none)
-  size_t lds_bytes_lds = 0, lds_bytes_gv = 0;
-  bool coop_lds = false, coop_gv = false;
-  // options
-  int64_t schedule = 0, wait_us = 10000000, xcd_remap = 1, v_staging = 0, passes = 1;
-  int64_t single_col = 1, lds_handover = 1;
-  // block trace: [2 p p] clock values of the last epoch (see bgmf_get_trace)
-  int64_t *d_trace = nullptr;
-  bool trace_valid = false;
-  // timing
-  hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
-  bool epoch_timed = false, rmse_timed = false;
-  int64_t chain[4] = {0, 0, 0, 0};
-  std::string msg;
-  // out-of-core: records in pinned host memory, streamed per stratum
-  int64_t budget = 0;            // device bytes for ratings (0: no limit)
-  bool ooc = false;
-  uint2 *host_rec = nullptr;     // stratum-major records (pinned)
-  int32_t *host_perm = nullptr;  // slot-order input positions (pinned)
-  uint2 *resident = nullptr;     // strata [0, s_res), copied once per load
-  int32_t s_res = 0;
-  uint2 *ring = nullptr;         // device slots of slot_recs records each
-  int nslots = 0;
-  int64_t slot_recs = 0;
-  std::vector<int64_t> strat;    // p + 1 record offsets of the strata
-  std::vector<int32_t> chunk;    // chunk c = strata [chunk[c], chunk[c + 1]), one slot each
-  size_t issued = 0;             // chunks whose copy has been queued in the current pass
-  hipStream_t side = nullptr;    // copies into the ring
-  std::vector<hipEvent_t> ready, freed;
-  std::vector<bool> slot_used;
-};
 
 namespace {
 
 thread_local std::string g_create_error;
+
+// Every device and pinned allocation of the library goes through these two,
+// which count them (BGMF_OPT_ALLOC_COUNT): a bound handle makes none in
+// bgmf_load_coo, bgmf_epoch or bgmf_rmse.
+hipError_t dev_alloc(bgmf_t *h, void **ptr, size_t bytes) {
+  ++h->alloc_calls;
+  return hipMalloc(ptr, bytes);
+}
+
+hipError_t pinned_alloc(bgmf_t *h, void **ptr, size_t bytes) {
+  ++h->alloc_calls;
+  return hipHostMalloc(ptr, bytes, hipHostMallocDefault);
+}
+
+constexpr size_t kAlign = 256;
+constexpr size_t aligned(size_t bytes) { return (bytes + kAlign - 1) & ~(kAlign - 1); }
+
+// Bump allocation inside one range of memory (a bound workspace or arena, or
+// one block the library allocated); every piece starts on a 256-byte
+// boundary, so a sequence of pieces fits in the sum of their aligned sizes.
+struct Carve {
+  char *base = nullptr;
+  size_t size = 0, used = 0, high = 0;
+  template <class T>
+  T *take(size_t count) {
+    const size_t off = aligned(used);
+    const size_t bytes = count * sizeof(T);
+    if (!base || off + bytes > size) return nullptr;
+    used = off + bytes;
+    high = std::max(high, used);
+    return reinterpret_cast<T *>(base + off);
+  }
+};
+
+// Sizes of a load (bytes).  Tables: block_ptr and, in-core, wblock_ptr
+// (p^2 + 1 int64 each) and the per-block row-repeat flags (p^2 bytes).
+size_t tables_bytes(int32_t p, bool wave_major) {
+  const size_t slots = (size_t)p * p;
+  return aligned((slots + 1) * 8) * (wave_major ? 2 : 1) + aligned(slots);
+}
+
+// In-core ratings: records and perm (kept), and the one-pass bucketing's
+// temporaries (the COO arrays on the device and the radix sort's scratch).
+size_t incore_keep_bytes(int64_t nnz) {
+  return aligned(((size_t)nnz + kRecPad) * 8) + aligned((size_t)nnz * 4);
+}
+size_t incore_temp_bytes(int64_t nnz, int32_t p) {
+  return 3 * aligned((size_t)nnz * 4) + aligned(bucket_scratch_bytes(nnz, (int64_t)p * p));
+}
+
+// Streamed load: the slot-count pass over batches of `batch` ratings ...
+size_t count_pass_bytes(int64_t batch, int32_t p) {
+  const int64_t slots = (int64_t)p * p;
+  return 2 * aligned((size_t)batch * 4) + aligned(((size_t)slots + 1) * 8) +
+         aligned(scan_scratch_bytes(slots));
+}
+// ... and the gathering and sorting of one group of at most `cap` ratings
+// in at most `span` consecutive slots.
+size_t group_pass_bytes(int64_t batch, int64_t cap, int64_t span) {
+  return 3 * aligned((size_t)batch * 4) + 2 * aligned(((size_t)batch + 1) * 8) +
+         aligned(scan_scratch_bytes(batch)) + 4 * aligned((size_t)cap * 4) + aligned(8) +
+         aligned(bucket_scratch_bytes(cap, span)) + aligned(((size_t)cap + kRecPad) * 8) +
+         aligned((size_t)cap * 4) + aligned(((size_t)span + 1) * 8);
+}
+size_t pinned_need_bytes(int64_t nnz) {
+  return aligned((size_t)nnz * 8) + aligned((size_t)nnz * 4);
+}
 
 // Zeroes the block trace with a kernel rather than a memset, so that an
 // epoch stays a sequence of kernel launches.
@@ -116,15 +123,12 @@ int fail(bgmf_t *h, int code, const char *fmt, ...) {
 
 void free_layout(bgmf_t *h) {
   if (h->side) hipStreamSynchronize(h->side);
-  hipFree(h->block_ptr);
-  hipFree(h->wblock_ptr);
-  hipFree(h->rowrep);
-  hipFree(h->perm);
-  hipFree(h->rec);
-  hipFree(h->ring);
-  hipFree(h->resident);
-  if (h->host_rec) hipHostFree(h->host_rec);
-  if (h->host_perm) hipHostFree(h->host_perm);
+  if (h->own_persist) hipFree(h->own_persist);
+  if (h->own_region) hipFree(h->own_region);
+  if (h->own_host) hipHostFree(h->own_host);
+  h->own_persist = nullptr;
+  h->own_region = nullptr;
+  h->own_host = nullptr;
   for (auto ev : h->ready) hipEventDestroy(ev);
   for (auto ev : h->freed) hipEventDestroy(ev);
   h->ready.clear();
@@ -231,6 +235,407 @@ int64_t check_cuts(const int64_t *cut, int32_t p, int64_t len, int64_t max_width
   return widest;
 }
 
+// Serial-chain statistics from the stratum-major block offsets.
+void set_chain_stats(bgmf_t *h, const std::vector<int64_t> &bp) {
+  const int64_t p = h->p;
+  std::vector<int64_t> colsum(p, 0), rowsum(p, 0);
+  int64_t barrier = 0, nonempty = 0;
+  for (int64_t s = 0; s < p; ++s) {
+    int64_t mx = 0;
+    for (int64_t R = 0; R < p; ++R) {
+      const int64_t c = bp[s * p + R + 1] - bp[s * p + R];
+      colsum[(R + s) % p] += c;
+      rowsum[R] += c;
+      mx = std::max(mx, c);
+      nonempty += c > 0;
+    }
+    barrier += mx;
+  }
+  h->chain[0] = *std::max_element(colsum.begin(), colsum.end());
+  h->chain[1] = *std::max_element(rowsum.begin(), rowsum.end());
+  h->chain[2] = barrier;
+  h->chain[3] = nonempty;
+}
+
+bool offsets_ok(const std::vector<int64_t> &bp, int64_t nnz) {
+  if (bp.front() != 0 || bp.back() != nnz) return false;
+  for (size_t q = 0; q + 1 < bp.size(); ++q)
+    if (bp[q] > bp[q + 1]) return false;
+  return true;
+}
+
+int layout_error(bgmf_t *h) {
+  hipMemset(h->err, 0, sizeof(int32_t));
+  free_layout(h);
+  return fail(h, BGMF_E_HIP, "internal error: the device bucketing produced an inconsistent layout");
+}
+
+// All ratings on the device: one bucketing pass over the whole input, records
+// in wave-major order.  Tables, records and perm are kept; the COO arrays and
+// the sort's scratch are temporaries (after the kept part of a bound
+// workspace, or one allocation freed before returning).
+int load_incore(bgmf_t *h, const int32_t *rows, const int32_t *cols, const float *vals,
+                int64_t nnz) {
+  const int64_t slots = (int64_t)h->p * h->p;
+  const size_t keep = tables_bytes(h->p, true) + incore_keep_bytes(nnz);
+  const size_t temp = incore_temp_bytes(nnz, h->p);
+  const size_t scratch_bytes = bucket_scratch_bytes(nnz, slots);
+  void *own_temp = nullptr;
+  Carve kc, tc;
+  if (h->bound) {
+    kc = Carve{h->ws, h->ws_bytes};
+  } else {
+    HIP_TRY(h, dev_alloc(h, &h->own_persist, keep));
+    kc = Carve{static_cast<char *>(h->own_persist), keep};
+    const hipError_t e = dev_alloc(h, &own_temp, temp);
+    if (e != hipSuccess) {
+      free_layout(h);
+      return fail(h, e == hipErrorOutOfMemory ? BGMF_E_NOMEM : BGMF_E_HIP,
+                  "hipMalloc(%zu bytes of bucketing temporaries): %s", temp, hipGetErrorString(e));
+    }
+    tc = Carve{static_cast<char *>(own_temp), temp};
+  }
+  h->block_ptr = kc.take<int64_t>(slots + 1);
+  h->wblock_ptr = kc.take<int64_t>(slots + 1);
+  h->rowrep = kc.take<uint8_t>(slots);
+  h->rec = kc.take<uint2>(nnz + kRecPad);
+  h->perm = kc.take<int32_t>(nnz);
+  if (h->bound) tc = Carve{h->ws, h->ws_bytes, kc.used, kc.used};
+  int32_t *d_rows = tc.take<int32_t>(nnz), *d_cols = tc.take<int32_t>(nnz);
+  float *d_vals = tc.take<float>(nnz);
+  void *scratch = tc.take<char>(scratch_bytes);
+  auto done = [&](int rc) {
+    if (own_temp) hipFree(own_temp);
+    own_temp = nullptr;
+    if (rc != BGMF_OK) free_layout(h);
+    return rc;
+  };
+  if (!h->block_ptr || !h->wblock_ptr || !h->rowrep || !h->rec || !h->perm || !d_rows ||
+      !d_cols || !d_vals || !scratch)
+    return done(fail(h, BGMF_E_HIP, "internal error: in-core load does not fit its plan"));
+  h->load_peak = (int64_t)(incore_keep_bytes(nnz) + temp);
+  h->load_groups = 0;
+#define LOAD_TRY(call)                                                                     \
+  do {                                                                                     \
+    hipError_t e_ = (call);                                                                \
+    if (e_ != hipSuccess)                                                                  \
+      return done(fail(h, e_ == hipErrorOutOfMemory ? BGMF_E_NOMEM : BGMF_E_HIP, "%s: %s", \
+                       #call, hipGetErrorString(e_)));                                     \
+  } while (0)
+  LOAD_TRY(hipMemcpyAsync(d_rows, rows, (size_t)nnz * sizeof(int32_t), hipMemcpyHostToDevice,
+                          h->stream));
+  LOAD_TRY(hipMemcpyAsync(d_cols, cols, (size_t)nnz * sizeof(int32_t), hipMemcpyHostToDevice,
+                          h->stream));
+  LOAD_TRY(hipMemcpyAsync(d_vals, vals, (size_t)nnz * sizeof(float), hipMemcpyHostToDevice,
+                          h->stream));
+  LOAD_TRY(hipMemsetAsync(h->err, 0, sizeof(int32_t), h->stream));
+  LOAD_TRY(hipMemsetAsync(h->rowrep, 0, (size_t)slots, h->stream));
+  BucketOut out{h->block_ptr, h->wblock_ptr, h->perm, h->rec, h->rowrep};
+  LOAD_TRY(bucket(d_rows, d_cols, d_vals, nnz, grid_of(h), h->rows_max, 0, slots, false,
+                  scratch, scratch_bytes, out, h->err, h->stream));
+  LOAD_TRY(hipStreamSynchronize(h->stream));
+  done(BGMF_OK);
+  int32_t derr = 0;
+  std::vector<int64_t> bp((size_t)slots + 1), wbp((size_t)slots + 1);
+  LOAD_TRY(hipMemcpy(&derr, h->err, sizeof derr, hipMemcpyDeviceToHost));
+  LOAD_TRY(hipMemcpy(bp.data(), h->block_ptr, bp.size() * sizeof(int64_t), hipMemcpyDeviceToHost));
+  LOAD_TRY(hipMemcpy(wbp.data(), h->wblock_ptr, wbp.size() * sizeof(int64_t),
+                     hipMemcpyDeviceToHost));
+#undef LOAD_TRY
+  // the sweep trusts these offsets: check them before any epoch may run
+  bool ok = derr == 0 && offsets_ok(bp, nnz) && offsets_ok(wbp, nnz);
+  for (int64_t b = 0; ok && b < h->p; ++b)
+    for (int64_t s2 = 0; ok && s2 < h->p; ++s2)
+      ok = wbp[b * h->p + s2 + 1] - wbp[b * h->p + s2] == bp[s2 * h->p + b + 1] - bp[s2 * h->p + b];
+  if (!ok) return layout_error(h);
+  set_chain_stats(h, bp);
+  return BGMF_OK;
+}
+
+// Ratings streamed from pinned host memory.  A pass over batches of the
+// input counts the ratings of every slot (block_ptr); the slots are then cut
+// into groups of whole blocks, and for each group a pass over the input
+// gathers its ratings in input order, sorts them on the device as a load of
+// its own and copies records and perm to their stratum-major place in
+// pinned memory.  (The input crosses the host link once per group, so a
+// small budget makes a slow load; the epochs do not depend on it.)  After
+// the load the same device region holds the ring of stream slots and the
+// resident strata, within `budget` bytes.  The bucketing's temporaries stay
+// within the bound workspace (after the tables), or, for a handle that
+// allocates its own memory, within max(budget, the bytes needed to bucket
+// the largest block).
+int load_streamed(bgmf_t *h, const int32_t *rows, const int32_t *cols, const float *vals,
+                  int64_t nnz, int64_t budget) {
+  const int32_t p = h->p;
+  const int64_t slots = (int64_t)p * p;
+  const size_t tab = tables_bytes(p, false);
+  const size_t hneed = pinned_need_bytes(nnz);
+  auto bail = [&](int code, const char *fmt, auto... args) {
+    free_layout(h);
+    return fail(h, code, fmt, args...);
+  };
+#define LOAD_TRY(call)                                                                    \
+  do {                                                                                    \
+    hipError_t e_ = (call);                                                               \
+    if (e_ != hipSuccess)                                                                 \
+      return bail(e_ == hipErrorOutOfMemory ? BGMF_E_NOMEM : BGMF_E_HIP, "%s: %s", #call, \
+                  hipGetErrorString(e_));                                                 \
+  } while (0)
+  Carve hc;
+  if (h->bound) {
+    if (!h->pinned || h->pinned_bytes < hneed)
+      return fail(h, BGMF_E_BUDGET,
+                  "the ratings do not fit the bound workspace, and streaming them needs a pinned "
+                  "host arena of %zu bytes (bound: %zu)",
+                  hneed, h->pinned ? h->pinned_bytes : (size_t)0);
+    hc = Carve{h->pinned, h->pinned_bytes};
+  } else {
+    LOAD_TRY(pinned_alloc(h, &h->own_host, hneed));
+    hc = Carve{static_cast<char *>(h->own_host), hneed};
+  }
+  h->host_rec = hc.take<uint2>(nnz);
+  h->host_perm = hc.take<int32_t>(nnz);
+  // block tables: the front of the workspace, or an allocation of their own
+  Carve tc;
+  if (h->bound) {
+    tc = Carve{h->ws, h->ws_bytes};
+  } else {
+    LOAD_TRY(dev_alloc(h, &h->own_persist, tab));
+    tc = Carve{static_cast<char *>(h->own_persist), tab};
+  }
+  h->block_ptr = tc.take<int64_t>(slots + 1);
+  h->rowrep = tc.take<uint8_t>(slots);
+  h->wblock_ptr = nullptr;
+  if (!h->host_rec || !h->host_perm || !h->block_ptr || !h->rowrep)
+    return bail(BGMF_E_HIP, "internal error: streamed load does not fit its plan");
+  // the ratings region: the rest of a bound workspace, or allocated per pass
+  const size_t ws_rest = h->bound ? h->ws_bytes - aligned(tc.used) : 0;
+  auto region = [&](size_t want, Carve *c) -> int {
+    if (h->bound) {
+      *c = Carve{h->ws + aligned(tc.used), ws_rest};
+      return BGMF_OK;
+    }
+    if (h->own_region) hipFree(h->own_region);
+    h->own_region = nullptr;
+    HIP_TRY(h, dev_alloc(h, &h->own_region, want));
+    *c = Carve{static_cast<char *>(h->own_region), want};
+    return BGMF_OK;
+  };
+  auto pick_batch = [&](auto bytes_of, size_t limit) {
+    int64_t batch = std::min<int64_t>(nnz, (int64_t)1 << 24);
+    while (batch > 4096 && bytes_of(batch) > limit) batch >>= 1;
+    return batch;
+  };
+  const Grid G = grid_of(h);
+  size_t peak = 0;
+
+  // pass 1: ratings per slot
+  {
+    const size_t limit =
+        h->bound ? ws_rest : std::max((size_t)budget, count_pass_bytes(std::min<int64_t>(nnz, 4096), p));
+    const int64_t batch = pick_batch([&](int64_t b) { return count_pass_bytes(b, p); }, limit);
+    const size_t want = count_pass_bytes(batch, p);
+    if (want > limit)
+      return bail(BGMF_E_BUDGET,
+                  "the bound workspace cannot hold the slot counts of a %d x %d grid (%zu bytes "
+                  "after the tables, %zu needed)",
+                  p, p, limit, want);
+    Carve c;
+    if (region(want, &c) != BGMF_OK) return bail(BGMF_E_NOMEM, "%s", h->msg.c_str());
+    int32_t *b_rows = c.take<int32_t>(batch), *b_cols = c.take<int32_t>(batch);
+    int64_t *count = c.take<int64_t>(slots + 1);
+    const size_t ssb = scan_scratch_bytes(slots);
+    void *ss = c.take<char>(ssb);
+    if (!b_rows || !b_cols || !count || !ss)
+      return bail(BGMF_E_HIP, "internal error: slot-count pass does not fit its plan");
+    peak = std::max(peak, c.high);
+    LOAD_TRY(hipMemsetAsync(count, 0, ((size_t)slots + 1) * sizeof(int64_t), h->stream));
+    for (int64_t e0 = 0; e0 < nnz; e0 += batch) {
+      const int64_t cnt = std::min(batch, nnz - e0);
+      LOAD_TRY(hipMemcpyAsync(b_rows, rows + e0, (size_t)cnt * 4, hipMemcpyHostToDevice, h->stream));
+      LOAD_TRY(hipMemcpyAsync(b_cols, cols + e0, (size_t)cnt * 4, hipMemcpyHostToDevice, h->stream));
+      LOAD_TRY(bucket_count_batch(b_rows, b_cols, cnt, G, count, h->stream));
+    }
+    LOAD_TRY(bucket_offsets(count, slots, h->block_ptr, ss, ssb, h->stream));
+    LOAD_TRY(hipStreamSynchronize(h->stream));
+  }
+  std::vector<int64_t> bp((size_t)slots + 1);
+  LOAD_TRY(hipMemcpy(bp.data(), h->block_ptr, bp.size() * sizeof(int64_t), hipMemcpyDeviceToHost));
+  if (!offsets_ok(bp, nnz)) return layout_error(h);
+
+  // ring of stream slots and resident strata, within the budget.
+  // The budget is split into a ring of 3 (else 2) slots and a resident
+  // region.  A slot holds the widest stratum plus the padding, and is made a
+  // quarter of the budget when that fits: each chunk of strata in a slot
+  // costs one copy and, with the persistent schedule, one launch, whose end
+  // is a barrier across all row-blocks, so few large chunks are better.  The
+  // resident region keeps the first strata of the epoch on the device for
+  // good; the ring streams the others, and their first copies run while the
+  // resident strata are swept.
+  h->strat.assign((size_t)p + 1, 0);
+  int64_t widest = 0;
+  for (int64_t s2 = 0; s2 <= p; ++s2) h->strat[s2] = bp[s2 * p];
+  for (int64_t s2 = 0; s2 < p; ++s2) widest = std::max(widest, h->strat[s2 + 1] - h->strat[s2]);
+  const int64_t need = widest + kRecPad;
+  const int64_t budget_recs = budget / (int64_t)sizeof(uint2);
+  h->nslots = 0;
+  for (int cand : {3, 2}) {
+    for (int64_t slot : {std::max(need, budget_recs / 4), need}) {
+      if ((int64_t)cand * slot <= budget_recs) {
+        h->nslots = cand;
+        h->slot_recs = slot;
+        break;
+      }
+    }
+    if (h->nslots) break;
+  }
+  if (h->nslots == 0)
+    return bail(BGMF_E_BUDGET,
+                "ratings budget of %lld bytes holds fewer than two strata (the widest stratum "
+                "needs %lld bytes)",
+                (long long)budget, (long long)(need * (int64_t)sizeof(uint2)));
+  const size_t ring_bytes = aligned((size_t)h->nslots * (size_t)h->slot_recs * sizeof(uint2));
+  const int64_t res_cap =
+      (size_t)budget > ring_bytes ? ((int64_t)((size_t)budget - ring_bytes)) / (int64_t)sizeof(uint2) : 0;
+  h->s_res = 0;
+  while (h->s_res < p && h->strat[h->s_res + 1] + kRecPad <= res_cap) ++h->s_res;
+  // chunks of consecutive streamed strata, each as many as fit in a slot
+  h->chunk.assign(1, h->s_res);
+  for (int32_t s2 = h->s_res; s2 < p; ++s2)
+    if (h->strat[s2 + 1] - h->strat[h->chunk.back()] + kRecPad > h->slot_recs)
+      h->chunk.push_back(s2);
+  if (h->chunk.back() != p) h->chunk.push_back(p);
+
+  // groups of whole blocks whose bucketing fits the region: at most `cap`
+  // ratings in at most `span` consecutive slots (the slot tables take up to
+  // a quarter of the region)
+  int64_t biggest = 1;
+  for (int64_t q = 0; q < slots; ++q) biggest = std::max(biggest, bp[q + 1] - bp[q]);
+  const int64_t min_batch = std::min<int64_t>(nnz, 4096);
+  const size_t limit =
+      h->bound ? ws_rest : std::max((size_t)budget, group_pass_bytes(min_batch, biggest, 1));
+  int64_t span = std::max<int64_t>(1, std::min<int64_t>(slots, (int64_t)(limit / 4 / 32)));
+  while (span > 1 && group_pass_bytes(min_batch, biggest, span) > limit) span >>= 1;
+  const int64_t batch =
+      pick_batch([&](int64_t b) { return group_pass_bytes(b, biggest, span); }, limit);
+  if (group_pass_bytes(batch, biggest, span) > limit)
+    return bail(BGMF_E_BUDGET,
+                "the largest block (%lld ratings) needs %zu bytes to be bucketed; the bound "
+                "workspace has %zu after the tables",
+                (long long)biggest, group_pass_bytes(batch, biggest, span), limit);
+  int64_t lo = biggest, hi = std::max<int64_t>(biggest, nnz);
+  while (lo < hi) {
+    const int64_t mid = lo + (hi - lo + 1) / 2;
+    if (group_pass_bytes(batch, mid, span) <= limit) lo = mid;
+    else hi = mid - 1;
+  }
+  const int64_t cap = lo;
+  std::vector<std::pair<int64_t, int64_t>> groups;
+  for (int64_t q0 = 0; q0 < slots;) {
+    int64_t q1 = q0 + 1;
+    while (q1 < slots && q1 - q0 < span && bp[q1 + 1] - bp[q0] <= cap) ++q1;
+    if (bp[q1] > bp[q0]) groups.emplace_back(q0, q1);
+    q0 = q1;
+  }
+  Carve dc;
+  if (region(std::max((size_t)budget, group_pass_bytes(batch, cap, span)), &dc) != BGMF_OK)
+    return bail(BGMF_E_NOMEM, "%s", h->msg.c_str());
+  const size_t mark = 0;
+  h->load_groups = (int64_t)groups.size();
+
+  // pass 2: gather, sort and store each group
+  {
+    Carve c = dc;
+    c.used = c.high = mark;
+    int32_t *b_rows = c.take<int32_t>(batch), *b_cols = c.take<int32_t>(batch);
+    float *b_vals = c.take<float>(batch);
+    int64_t *flag = c.take<int64_t>(batch + 1), *pos = c.take<int64_t>(batch + 1);
+    const size_t ssb = scan_scratch_bytes(batch);
+    void *ss = c.take<char>(ssb);
+    GroupArrays g{c.take<int32_t>(cap), c.take<int32_t>(cap), c.take<float>(cap),
+                  c.take<int32_t>(cap), cap};
+    int64_t *fill = c.take<int64_t>(1);
+    const size_t bsb = bucket_scratch_bytes(cap, span);
+    void *bs = c.take<char>(bsb);
+    uint2 *rec_t = c.take<uint2>(cap + kRecPad);
+    int32_t *perm_t = c.take<int32_t>(cap);
+    int64_t *bp_t = c.take<int64_t>(span + 1);
+    if (!b_rows || !b_cols || !b_vals || !flag || !pos || !ss || !g.rows || !g.cols || !g.vals ||
+        !g.e || !fill || !bs || !rec_t || !perm_t || !bp_t)
+      return bail(BGMF_E_HIP, "internal error: group pass does not fit its plan");
+    peak = std::max(peak, c.high);
+    LOAD_TRY(hipMemsetAsync(h->err, 0, sizeof(int32_t), h->stream));
+    LOAD_TRY(hipMemsetAsync(h->rowrep, 0, (size_t)slots, h->stream));
+    std::vector<int64_t> got;
+    for (const auto &gr : groups) {
+      const int64_t q0 = gr.first, q1 = gr.second, gcnt = bp[q1] - bp[q0];
+      LOAD_TRY(hipMemsetAsync(fill, 0, sizeof(int64_t), h->stream));
+      for (int64_t e0 = 0; e0 < nnz; e0 += batch) {
+        const int64_t cnt = std::min(batch, nnz - e0);
+        LOAD_TRY(hipMemcpyAsync(b_rows, rows + e0, (size_t)cnt * 4, hipMemcpyHostToDevice, h->stream));
+        LOAD_TRY(hipMemcpyAsync(b_cols, cols + e0, (size_t)cnt * 4, hipMemcpyHostToDevice, h->stream));
+        LOAD_TRY(hipMemcpyAsync(b_vals, vals + e0, (size_t)cnt * 4, hipMemcpyHostToDevice, h->stream));
+        LOAD_TRY(bucket_select_batch(b_rows, b_cols, b_vals, cnt, e0, G, q0, q1, flag, pos, ss,
+                                     ssb, fill, g, h->err, h->stream));
+      }
+      BucketOut out{bp_t, nullptr, perm_t, rec_t, h->rowrep};
+      LOAD_TRY(bucket(g.rows, g.cols, g.vals, gcnt, G, h->rows_max, q0, q1 - q0, true, bs, bsb,
+                      out, h->err, h->stream));
+      LOAD_TRY(bucket_map_perm(perm_t, g.e, gcnt, h->err, h->stream));
+      LOAD_TRY(hipMemcpyAsync(h->host_rec + bp[q0], rec_t, (size_t)gcnt * sizeof(uint2),
+                              hipMemcpyDeviceToHost, h->stream));
+      LOAD_TRY(hipMemcpyAsync(h->host_perm + bp[q0], perm_t, (size_t)gcnt * sizeof(int32_t),
+                              hipMemcpyDeviceToHost, h->stream));
+      // the group's own offsets must agree with the counting pass
+      got.assign((size_t)(q1 - q0) + 2, -1);
+      LOAD_TRY(hipMemcpyAsync(got.data(), bp_t, (size_t)(q1 - q0 + 1) * sizeof(int64_t),
+                              hipMemcpyDeviceToHost, h->stream));
+      LOAD_TRY(hipMemcpyAsync(got.data() + (q1 - q0 + 1), fill, sizeof(int64_t),
+                              hipMemcpyDeviceToHost, h->stream));
+      LOAD_TRY(hipStreamSynchronize(h->stream));
+      bool ok = got[q1 - q0 + 1] == gcnt;
+      for (int64_t q = q0; ok && q <= q1; ++q) ok = got[q - q0] - got[0] == bp[q] - bp[q0];
+      if (!ok) return layout_error(h);
+    }
+    int32_t derr = 0;
+    LOAD_TRY(hipMemcpy(&derr, h->err, sizeof derr, hipMemcpyDeviceToHost));
+    if (derr != 0) return layout_error(h);
+  }
+
+  // the region now holds the ring and the resident strata
+  {
+    Carve c = dc;
+    c.used = c.high = mark;
+    const int64_t count = h->strat[h->s_res];
+    h->ring = c.take<uint2>((size_t)h->nslots * (size_t)h->slot_recs);
+    h->resident = h->s_res > 0 ? c.take<uint2>((size_t)count + kRecPad) : nullptr;
+    if (!h->ring || (h->s_res > 0 && !h->resident))
+      return bail(BGMF_E_HIP, "internal error: stream ring does not fit its plan");
+    peak = std::max(peak, c.high);
+    if (h->s_res > 0) {
+      LOAD_TRY(hipMemcpyAsync(h->resident, h->host_rec, (size_t)count * sizeof(uint2),
+                              hipMemcpyHostToDevice, h->stream));
+      LOAD_TRY(hipMemsetAsync(h->resident + count, 0, (size_t)kRecPad * sizeof(uint2), h->stream));
+    }
+    LOAD_TRY(hipMemsetAsync(h->ring, 0, (size_t)h->nslots * (size_t)h->slot_recs * sizeof(uint2),
+                            h->stream));
+  }
+  if (!h->side) LOAD_TRY(hipStreamCreateWithFlags(&h->side, hipStreamNonBlocking));
+  h->ready.assign(h->nslots, nullptr);
+  h->freed.assign(h->nslots, nullptr);
+  h->slot_used.assign(h->nslots, false);
+  for (int i = 0; i < h->nslots; ++i) {
+    LOAD_TRY(hipEventCreateWithFlags(&h->ready[i], hipEventDisableTiming));
+    LOAD_TRY(hipEventCreateWithFlags(&h->freed[i], hipEventDisableTiming));
+  }
+  LOAD_TRY(hipStreamSynchronize(h->stream));
+#undef LOAD_TRY
+  h->load_peak = (int64_t)peak;
+  h->ooc = true;
+  set_chain_stats(h, bp);
+  return BGMF_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -290,8 +695,13 @@ bgmf_t *bgmf_create(int64_t n, int64_t m, int32_t k, int32_t p) {
       hipSuccess)
     return bail(e, "hipDeviceGetAttribute");
   h->lds_limit = (size_t)lds_max;
+  int khz = 0;
+  if ((e = hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, h->device)) != hipSuccess)
+    return bail(e, "hipDeviceGetAttribute");
+  if (khz > 0) h->clock_khz = khz;
   if ((e = configure_sweep(h)) != hipSuccess) return bail(e, "configure_sweep");
-  if ((e = hipMalloc(&h->d_cuts, 2 * ((size_t)p + 1) * sizeof(int64_t))) != hipSuccess)
+  if ((e = dev_alloc(h, reinterpret_cast<void **>(&h->d_cuts),
+                     2 * ((size_t)p + 1) * sizeof(int64_t))) != hipSuccess)
     return bail(e, "hipMalloc(cuts)");
   if ((e = hipMemcpy(h->d_cuts, h->rcut.data(), ((size_t)p + 1) * sizeof(int64_t),
                      hipMemcpyHostToDevice)) != hipSuccess ||
@@ -303,22 +713,26 @@ bgmf_t *bgmf_create(int64_t n, int64_t m, int32_t k, int32_t p) {
   h->stream = h->own_stream;
   for (auto &ev : h->ev)
     if ((e = hipEventCreate(&ev)) != hipSuccess) return bail(e, "hipEventCreate");
-  // one spare row after U absorbs the padding steps of the sweep
-  if ((e = hipMalloc(&h->U, (size_t)(n + 1) * k * sizeof(float))) != hipSuccess)
+  if ((e = dev_alloc(h, reinterpret_cast<void **>(&h->U), (size_t)n * k * sizeof(float))) !=
+      hipSuccess)
     return bail(e, "hipMalloc(U)");
-  if ((e = hipMalloc(&h->V, (size_t)m * k * sizeof(float))) != hipSuccess)
+  if ((e = dev_alloc(h, reinterpret_cast<void **>(&h->V), (size_t)m * k * sizeof(float))) !=
+      hipSuccess)
     return bail(e, "hipMalloc(V)");
-  if ((e = hipMalloc(&h->flags, (size_t)p * kFlagStride * sizeof(int64_t))) != hipSuccess)
+  if ((e = dev_alloc(h, reinterpret_cast<void **>(&h->flags),
+                     (size_t)p * kFlagStride * sizeof(int64_t))) != hipSuccess)
     return bail(e, "hipMalloc(flags)");
-  if ((e = hipMalloc(&h->err, sizeof(int32_t))) != hipSuccess) return bail(e, "hipMalloc(err)");
-  if ((e = hipMalloc(&h->partials, rmse_partials_count(p) * sizeof(double))) != hipSuccess)
+  if ((e = dev_alloc(h, reinterpret_cast<void **>(&h->err), sizeof(int32_t))) != hipSuccess)
+    return bail(e, "hipMalloc(err)");
+  if ((e = dev_alloc(h, reinterpret_cast<void **>(&h->partials),
+                     rmse_partials_count(p) * sizeof(double))) != hipSuccess)
     return bail(e, "hipMalloc(partials)");
-  if ((e = hipMalloc(&h->d_rmse, sizeof(double))) != hipSuccess)
+  if ((e = dev_alloc(h, reinterpret_cast<void **>(&h->d_rmse), sizeof(double))) != hipSuccess)
     return bail(e, "hipMalloc(rmse)");
   if ((e = hipMemset(h->flags, 0, (size_t)p * kFlagStride * sizeof(int64_t))) != hipSuccess)
     return bail(e, "hipMemset");
   if ((e = hipMemset(h->err, 0, sizeof(int32_t))) != hipSuccess) return bail(e, "hipMemset");
-  if ((e = hipMemset(h->U, 0, (size_t)(n + 1) * k * sizeof(float))) != hipSuccess)
+  if ((e = hipMemset(h->U, 0, (size_t)n * k * sizeof(float))) != hipSuccess)
     return bail(e, "hipMemset");
   if ((e = hipMemset(h->V, 0, (size_t)m * k * sizeof(float))) != hipSuccess)
     return bail(e, "hipMemset");
@@ -329,8 +743,10 @@ void bgmf_destroy(bgmf_t *h) {
   if (!h) return;
   if (h->stream) hipStreamSynchronize(h->stream);
   free_layout(h);
-  hipFree(h->U);
-  hipFree(h->V);
+  if (h->own_factors) {
+    hipFree(h->U);
+    hipFree(h->V);
+  }
   hipFree(h->flags);
   hipFree(h->err);
   hipFree(h->partials);
@@ -356,6 +772,86 @@ int bgmf_set_stream(bgmf_t *h, void *hip_stream) {
     HIP_TRY(h, hipStreamSynchronize(h->stream));
     h->stream = next;
   }
+  return BGMF_OK;
+}
+
+int bgmf_query_sizes(const bgmf_t *h, int64_t nnz, size_t *factor_bytes, size_t *min_ws_bytes,
+                     size_t *incore_ws_bytes, size_t *pinned_bytes) {
+  if (!h) return BGMF_E_ARG;
+  if (nnz < 1 || nnz >= (1ll << 31)) {
+    const_cast<bgmf_t *>(h)->msg = "bgmf_query_sizes: nnz must be in [1, 2^31)";
+    return BGMF_E_ARG;
+  }
+  const int32_t p = h->p;
+  if (factor_bytes) *factor_bytes = (size_t)(h->n + h->m) * (size_t)h->k * sizeof(float);
+  if (incore_ws_bytes)
+    *incore_ws_bytes = tables_bytes(p, true) + incore_keep_bytes(nnz) + incore_temp_bytes(nnz, p);
+  if (min_ws_bytes) {
+    // necessary, not sufficient: the streamed load also needs room to bucket
+    // its largest block and a ring of two copies of its widest stratum, which
+    // depend on how the ratings fall into the grid
+    const int64_t slots = (int64_t)p * p;
+    const int64_t per_stratum = (nnz + p - 1) / p, per_block = (nnz + slots - 1) / slots;
+    int64_t batch = std::min<int64_t>(nnz, 4096);
+    size_t need = std::max(count_pass_bytes(batch, p), group_pass_bytes(batch, per_block, 1));
+    need = std::max(need, 2 * aligned(((size_t)per_stratum + kRecPad) * sizeof(uint2)) + 2 * kAlign);
+    *min_ws_bytes = tables_bytes(p, false) + need;
+  }
+  if (pinned_bytes) *pinned_bytes = pinned_need_bytes(nnz);
+  return BGMF_OK;
+}
+
+int bgmf_bind(bgmf_t *h, float *U_dev, float *V_dev, void *ws_dev, size_t ws_bytes,
+              void *pinned_host, size_t pinned_bytes, void *hip_stream) {
+  if (!h) return BGMF_E_ARG;
+  if (!U_dev || !V_dev || !ws_dev)
+    return fail(h, BGMF_E_ARG, "bgmf_bind: U, V and the workspace must be given");
+  const uintptr_t bits = reinterpret_cast<uintptr_t>(U_dev) | reinterpret_cast<uintptr_t>(V_dev) |
+                         reinterpret_cast<uintptr_t>(ws_dev) |
+                         reinterpret_cast<uintptr_t>(pinned_host);
+  if (bits & (kAlign - 1))
+    return fail(h, BGMF_E_ARG, "bgmf_bind: every buffer must start on a 256-byte boundary");
+  if (pinned_host == nullptr) pinned_bytes = 0;
+  if (h->loaded) return fail(h, BGMF_E_STATE, "bgmf_bind: bind before loading ratings");
+  if (ws_bytes < tables_bytes(h->p, false))
+    return fail(h, BGMF_E_BUDGET, "bgmf_bind: a workspace of %zu bytes is smaller than the "
+                "block tables (%zu bytes)", ws_bytes, tables_bytes(h->p, false));
+  // the buffers must be memory the device can reach: device memory on the
+  // handle's device, and pinned host memory for the arena
+  for (const void *ptr : {static_cast<const void *>(U_dev), static_cast<const void *>(V_dev),
+                          static_cast<const void *>(ws_dev)}) {
+    hipPointerAttribute_t a{};
+    if (hipPointerGetAttributes(&a, ptr) != hipSuccess || a.type != hipMemoryTypeDevice ||
+        a.device != h->device) {
+      hipGetLastError();
+      return fail(h, BGMF_E_ARG, "bgmf_bind: U, V and the workspace must be device memory on "
+                  "device %d", h->device);
+    }
+  }
+  if (pinned_host) {
+    hipPointerAttribute_t a{};
+    if (hipPointerGetAttributes(&a, pinned_host) != hipSuccess || a.type != hipMemoryTypeHost) {
+      hipGetLastError();
+      return fail(h, BGMF_E_ARG, "bgmf_bind: the host arena must be pinned host memory");
+    }
+  }
+  int rc = bgmf_set_stream(h, hip_stream);
+  if (rc != BGMF_OK) return rc;
+  HIP_TRY(h, hipStreamSynchronize(h->stream));
+  free_layout(h);
+  if (h->own_factors) {
+    hipFree(h->U);
+    hipFree(h->V);
+  }
+  h->U = U_dev;
+  h->V = V_dev;
+  h->own_factors = false;
+  h->factors_set = true;  // the caller's buffers hold the factors
+  h->bound = true;
+  h->ws = static_cast<char *>(ws_dev);
+  h->ws_bytes = ws_bytes;
+  h->pinned = static_cast<char *>(pinned_host);
+  h->pinned_bytes = pinned_bytes;
   return BGMF_OK;
 }
 
@@ -390,169 +886,24 @@ int bgmf_load_coo(bgmf_t *h, const int32_t *rows, const int32_t *cols, const flo
   }
   HIP_TRY(h, hipStreamSynchronize(h->stream));
   free_layout(h);
-
-  const int64_t slots = (int64_t)h->p * h->p;
-  int32_t *d_rows = nullptr, *d_cols = nullptr;
-  float *d_vals = nullptr;
-  void *scratch = nullptr;
-  const size_t scratch_bytes = bucket_scratch_bytes(nnz, h->p);
-  int rc = BGMF_OK;
-  auto cleanup = [&]() {
-    hipFree(d_rows);
-    hipFree(d_cols);
-    hipFree(d_vals);
-    hipFree(scratch);
-  };
-#define LOAD_TRY(call)                                                                     \
-  do {                                                                                     \
-    hipError_t e_ = (call);                                                                \
-    if (e_ != hipSuccess) {                                                                \
-      rc = fail(h, e_ == hipErrorOutOfMemory ? BGMF_E_NOMEM : BGMF_E_HIP, "%s: %s", #call, \
-                hipGetErrorString(e_));                                                    \
-      cleanup();                                                                           \
-      free_layout(h);                                                                      \
-      return rc;                                                                           \
-    }                                                                                      \
-  } while (0)
-  LOAD_TRY(hipMalloc(&d_rows, (size_t)nnz * sizeof(int32_t)));
-  LOAD_TRY(hipMalloc(&d_cols, (size_t)nnz * sizeof(int32_t)));
-  LOAD_TRY(hipMalloc(&d_vals, (size_t)nnz * sizeof(float)));
-  LOAD_TRY(hipMalloc(&scratch, scratch_bytes));
-  LOAD_TRY(hipMalloc(&h->block_ptr, (size_t)(slots + 1) * sizeof(int64_t)));
-  LOAD_TRY(hipMalloc(&h->wblock_ptr, (size_t)(slots + 1) * sizeof(int64_t)));
-  LOAD_TRY(hipMalloc(&h->rowrep, (size_t)slots));
-  LOAD_TRY(hipMalloc(&h->perm, (size_t)nnz * sizeof(int32_t)));
-  LOAD_TRY(hipMalloc(&h->rec, (size_t)(nnz + kRecPad) * sizeof(uint2)));
-  LOAD_TRY(hipMemcpyAsync(d_rows, rows, (size_t)nnz * sizeof(int32_t), hipMemcpyHostToDevice,
-                          h->stream));
-  LOAD_TRY(hipMemcpyAsync(d_cols, cols, (size_t)nnz * sizeof(int32_t), hipMemcpyHostToDevice,
-                          h->stream));
-  LOAD_TRY(hipMemcpyAsync(d_vals, vals, (size_t)nnz * sizeof(float), hipMemcpyHostToDevice,
-                          h->stream));
-  BucketOut out{h->block_ptr, h->wblock_ptr, h->perm, h->rec, h->rowrep};
-  LOAD_TRY(hipMemsetAsync(h->err, 0, sizeof(int32_t), h->stream));
-  LOAD_TRY(hipMemsetAsync(h->rowrep, 0, (size_t)slots, h->stream));
-  // ratings that do not fit the budget are kept stratum-major, so that each
-  // stratum is one contiguous range to stream
-  const bool ooc = h->budget > 0 && (nnz + kRecPad) * (int64_t)sizeof(uint2) > h->budget;
-  LOAD_TRY(bucket(d_rows, d_cols, d_vals, nnz, grid_of(h), h->rows_max, ooc, scratch,
-                  scratch_bytes, out, h->err, h->stream));
-  LOAD_TRY(hipStreamSynchronize(h->stream));
-  cleanup();
-#undef LOAD_TRY
-  int32_t derr = 0;
-  HIP_TRY(h, hipMemcpy(&derr, h->err, sizeof derr, hipMemcpyDeviceToHost));
-
-  // serial-chain statistics from the block sizes
-  std::vector<int64_t> bp((size_t)slots + 1), wbp((size_t)slots + 1);
-  HIP_TRY(h, hipMemcpy(bp.data(), h->block_ptr, bp.size() * sizeof(int64_t),
-                       hipMemcpyDeviceToHost));
-  HIP_TRY(h, hipMemcpy(wbp.data(), h->wblock_ptr, wbp.size() * sizeof(int64_t),
-                       hipMemcpyDeviceToHost));
-  // the sweep trusts these offsets: check them before any epoch may run
-  bool ok = derr == 0 && bp[0] == 0 && wbp[0] == 0 && bp[slots] == nnz && wbp[slots] == nnz;
-  for (int64_t q = 0; ok && q < slots; ++q) ok = bp[q] <= bp[q + 1] && wbp[q] <= wbp[q + 1];
-  for (int64_t b = 0; ok && b < h->p; ++b)
-    for (int64_t s2 = 0; ok && s2 < h->p; ++s2)
-      ok = wbp[b * h->p + s2 + 1] - wbp[b * h->p + s2] == bp[s2 * h->p + b + 1] - bp[s2 * h->p + b];
-  if (!ok) {
-    hipMemset(h->err, 0, sizeof(int32_t));
-    free_layout(h);
-    return fail(h, BGMF_E_HIP, "internal error: the device bucketing produced an inconsistent layout");
+  // In-core when the one-pass bucketing (records, perm and its temporaries)
+  // fits the ratings budget -- a bound workspace minus the tables, or the
+  // BGMF_OPT_RATINGS_BUDGET option, whichever is smaller -- else streamed.
+  const size_t incore = incore_keep_bytes(nnz) + incore_temp_bytes(nnz, h->p);
+  int64_t region = h->budget;  // 0: no limit
+  bool fits = h->budget == 0 || incore <= (size_t)h->budget;
+  if (h->bound) {
+    const size_t tab_in = tables_bytes(h->p, true), tab_st = tables_bytes(h->p, false);
+    fits = fits && h->ws_bytes >= tab_in + incore;
+    if (h->ws_bytes < tab_st)
+      return fail(h, BGMF_E_BUDGET, "the bound workspace (%zu bytes) is smaller than the block "
+                  "tables (%zu bytes)", h->ws_bytes, tab_st);
+    const int64_t avail = (int64_t)(h->ws_bytes - tab_st);
+    region = h->budget > 0 ? std::min(h->budget, avail) : avail;
   }
-  std::vector<int64_t> colsum(h->p, 0), rowsum(h->p, 0);
-  int64_t barrier = 0, nonempty = 0;
-  for (int64_t s = 0; s < h->p; ++s) {
-    int64_t mx = 0;
-    for (int64_t R = 0; R < h->p; ++R) {
-      const int64_t c = bp[s * h->p + R + 1] - bp[s * h->p + R];
-      colsum[(R + s) % h->p] += c;
-      rowsum[R] += c;
-      mx = std::max(mx, c);
-      nonempty += c > 0;
-    }
-    barrier += mx;
-  }
-  h->chain[0] = *std::max_element(colsum.begin(), colsum.end());
-  h->chain[1] = *std::max_element(rowsum.begin(), rowsum.end());
-  h->chain[2] = barrier;
-  h->chain[3] = nonempty;
-
-  if (ooc) {
-    h->strat.assign((size_t)h->p + 1, 0);
-    int64_t widest = 0;
-    for (int64_t s2 = 0; s2 <= h->p; ++s2) h->strat[s2] = bp[s2 * h->p];
-    for (int64_t s2 = 0; s2 < h->p; ++s2) widest = std::max(widest, h->strat[s2 + 1] - h->strat[s2]);
-    // The budget is split into a ring of 3 (else 2) slots and a resident
-    // region.  A slot holds the widest stratum plus the padding, and is made
-    // a quarter of the budget when that fits: each chunk of strata in a slot
-    // costs one copy and, with the persistent schedule, one launch, whose
-    // end is a barrier across all row-blocks, so few large chunks are
-    // better.  The resident region keeps the first strata of the epoch on
-    // the device for good; the ring streams the others, and their first
-    // copies run while the resident strata are swept.
-    const int64_t need = widest + kRecPad;
-    const int64_t budget_recs = h->budget / (int64_t)sizeof(uint2);
-    h->nslots = 0;
-    for (int cand : {3, 2}) {
-      for (int64_t slot : {std::max(need, budget_recs / 4), need}) {
-        if ((int64_t)cand * slot <= budget_recs) {
-          h->nslots = cand;
-          h->slot_recs = slot;
-          break;
-        }
-      }
-      if (h->nslots) break;
-    }
-    if (h->nslots == 0) {
-      const int64_t slot_bytes = need * (int64_t)sizeof(uint2);
-      free_layout(h);
-      return fail(h, BGMF_E_BUDGET,
-                  "ratings budget of %lld bytes holds fewer than two strata (the widest stratum "
-                  "needs %lld bytes)",
-                  (long long)h->budget, (long long)slot_bytes);
-    }
-    const int64_t res_cap = budget_recs - (int64_t)h->nslots * h->slot_recs;
-    h->s_res = 0;
-    while (h->s_res < h->p && h->strat[h->s_res + 1] + kRecPad <= res_cap) ++h->s_res;
-    // chunks of consecutive streamed strata, each as many as fit in a slot
-    h->chunk.assign(1, h->s_res);
-    for (int32_t s2 = h->s_res; s2 < h->p; ++s2)
-      if (h->strat[s2 + 1] - h->strat[h->chunk.back()] + kRecPad > h->slot_recs)
-        h->chunk.push_back(s2);
-    if (h->chunk.back() != h->p) h->chunk.push_back(h->p);
-    const int64_t slot_bytes = h->slot_recs * (int64_t)sizeof(uint2);
-    if (!h->side) HIP_TRY(h, hipStreamCreateWithFlags(&h->side, hipStreamNonBlocking));
-    HIP_TRY(h, hipHostMalloc(reinterpret_cast<void **>(&h->host_rec),
-                             (size_t)nnz * sizeof(uint2), hipHostMallocDefault));
-    HIP_TRY(h, hipHostMalloc(reinterpret_cast<void **>(&h->host_perm),
-                             (size_t)nnz * sizeof(int32_t), hipHostMallocDefault));
-    HIP_TRY(h, hipMemcpy(h->host_rec, h->rec, (size_t)nnz * sizeof(uint2), hipMemcpyDeviceToHost));
-    HIP_TRY(h, hipMemcpy(h->host_perm, h->perm, (size_t)nnz * sizeof(int32_t),
-                         hipMemcpyDeviceToHost));
-    hipFree(h->rec);
-    hipFree(h->perm);
-    h->rec = nullptr;
-    h->perm = nullptr;
-    if (h->s_res > 0) {
-      const int64_t count = h->strat[h->s_res];
-      HIP_TRY(h, hipMalloc(&h->resident, (size_t)(count + kRecPad) * sizeof(uint2)));
-      HIP_TRY(h, hipMemcpy(h->resident, h->host_rec, (size_t)count * sizeof(uint2),
-                           hipMemcpyHostToDevice));
-      HIP_TRY(h, hipMemset(h->resident + count, 0, (size_t)kRecPad * sizeof(uint2)));
-    }
-    HIP_TRY(h, hipMalloc(&h->ring, (size_t)h->nslots * (size_t)slot_bytes));
-    HIP_TRY(h, hipMemset(h->ring, 0, (size_t)h->nslots * (size_t)slot_bytes));
-    h->ready.assign(h->nslots, nullptr);
-    h->freed.assign(h->nslots, nullptr);
-    h->slot_used.assign(h->nslots, false);
-    for (int i = 0; i < h->nslots; ++i) {
-      HIP_TRY(h, hipEventCreateWithFlags(&h->ready[i], hipEventDisableTiming));
-      HIP_TRY(h, hipEventCreateWithFlags(&h->freed[i], hipEventDisableTiming));
-    }
-    h->ooc = true;
-  }
-
+  const int rc = fits ? load_incore(h, rows, cols, vals, nnz)
+                      : load_streamed(h, rows, cols, vals, nnz, region);
+  if (rc != BGMF_OK) return rc;
   HIP_TRY(h, hipMemsetAsync(h->flags, 0, (size_t)h->p * kFlagStride * sizeof(int64_t), h->stream));
   HIP_TRY(h, hipStreamSynchronize(h->stream));
   h->epochs_done = 0;
@@ -662,7 +1013,7 @@ int bgmf_epoch(bgmf_t *h, float alpha, float beta) {
   P.p = h->p;
   P.cols_max = h->cols_max;
   P.g_base = h->epochs_done * (int64_t)h->p;
-  P.wait_ticks = h->wait_us * 100;  // s_memrealtime runs at 100 MHz
+  P.wait_ticks = h->wait_us * h->clock_khz / 1000;  // s_memrealtime ticks
   P.alpha = alpha;
   P.beta = beta;
   P.xcd_remap = (int32_t)h->xcd_remap;
@@ -890,17 +1241,22 @@ int bgmf_rmse_coo(bgmf_t *h, const int32_t *rows, const int32_t *cols, const flo
   double r = 0.0;
   hipError_t e = hipSuccess;
   const size_t np = rmse_coo_partials_count();
-  if ((e = hipMalloc(&d_rows, (size_t)nnz * sizeof(int32_t))) == hipSuccess &&
-      (e = hipMalloc(&d_cols, (size_t)nnz * sizeof(int32_t))) == hipSuccess &&
-      (e = hipMalloc(&d_vals, (size_t)nnz * sizeof(float))) == hipSuccess &&
-      (e = hipMalloc(&d_part, (np + 1) * sizeof(double))) == hipSuccess &&
+  if ((e = dev_alloc(h, reinterpret_cast<void **>(&d_rows), (size_t)nnz * sizeof(int32_t))) ==
+          hipSuccess &&
+      (e = dev_alloc(h, reinterpret_cast<void **>(&d_cols), (size_t)nnz * sizeof(int32_t))) ==
+          hipSuccess &&
+      (e = dev_alloc(h, reinterpret_cast<void **>(&d_vals), (size_t)nnz * sizeof(float))) ==
+          hipSuccess &&
+      (e = dev_alloc(h, reinterpret_cast<void **>(&d_part), (np + 2) * sizeof(double))) ==
+          hipSuccess &&
       (e = hipMemcpyAsync(d_rows, rows, (size_t)nnz * sizeof(int32_t), hipMemcpyHostToDevice,
                           h->stream)) == hipSuccess &&
       (e = hipMemcpyAsync(d_cols, cols, (size_t)nnz * sizeof(int32_t), hipMemcpyHostToDevice,
                           h->stream)) == hipSuccess &&
       (e = hipMemcpyAsync(d_vals, vals, (size_t)nnz * sizeof(float), hipMemcpyHostToDevice,
                           h->stream)) == hipSuccess &&
-      (e = launch_rmse_coo(d_rows, d_cols, d_vals, nnz, h->U, h->V, h->k, d_part, d_part + np,
+      (e = launch_rmse_coo(d_rows, d_cols, d_vals, nnz, h->U, h->V, h->k, h->n, h->m, d_part,
+                           d_part + np, reinterpret_cast<int32_t *>(d_part + np + 1),
                            h->stream)) == hipSuccess &&
       (e = hipMemcpyAsync(&r, d_part + np, sizeof r, hipMemcpyDeviceToHost, h->stream)) ==
           hipSuccess)
@@ -1031,11 +1387,18 @@ int bgmf_set_option(bgmf_t *h, int32_t option, int64_t value) {
       return fail(h, BGMF_E_ARG, "BGMF_OPT_STREAM_CHUNKS is read-only");
     case BGMF_OPT_RESIDENT_STRATA:
       return fail(h, BGMF_E_ARG, "BGMF_OPT_RESIDENT_STRATA is read-only");
+    case BGMF_OPT_ALLOC_COUNT:
+      return fail(h, BGMF_E_ARG, "BGMF_OPT_ALLOC_COUNT is read-only");
+    case BGMF_OPT_LOAD_PEAK:
+      return fail(h, BGMF_E_ARG, "BGMF_OPT_LOAD_PEAK is read-only");
+    case BGMF_OPT_LOAD_GROUPS:
+      return fail(h, BGMF_E_ARG, "BGMF_OPT_LOAD_GROUPS is read-only");
     case BGMF_OPT_TRACE:
       if (value != 0 && value != 1) return fail(h, BGMF_E_ARG, "trace must be 0 or 1");
       if (value == 1 && !h->d_trace) {
         HIP_TRY(h, hipStreamSynchronize(h->stream));
-        HIP_TRY(h, hipMalloc(&h->d_trace, 2 * (size_t)h->p * h->p * sizeof(int64_t)));
+        HIP_TRY(h, dev_alloc(h, reinterpret_cast<void **>(&h->d_trace),
+                             2 * (size_t)h->p * h->p * sizeof(int64_t)));
       } else if (value == 0 && h->d_trace) {
         HIP_TRY(h, hipStreamSynchronize(h->stream));
         HIP_TRY(h, hipFree(h->d_trace));
@@ -1065,6 +1428,9 @@ int bgmf_get_option(const bgmf_t *h, int32_t option, int64_t *value) {
     case BGMF_OPT_SINGLE_COLUMN: *value = h->single_col; return BGMF_OK;
     case BGMF_OPT_LDS_HANDOVER: *value = h->lds_handover; return BGMF_OK;
     case BGMF_OPT_TRACE: *value = h->d_trace ? 1 : 0; return BGMF_OK;
+    case BGMF_OPT_ALLOC_COUNT: *value = h->alloc_calls; return BGMF_OK;
+    case BGMF_OPT_LOAD_PEAK: *value = h->load_peak; return BGMF_OK;
+    case BGMF_OPT_LOAD_GROUPS: *value = h->load_groups; return BGMF_OK;
     case BGMF_OPT_PLACEMENT: {
       const SweepShape sh = sweep_shape(h);
       *value = (sh.lds ? 1 : 2) | (sh.persistent ? 4 : 0);
@@ -1110,9 +1476,7 @@ int bgmf_get_trace(bgmf_t *h, int64_t *begin, int64_t *end, int64_t *ticks_per_s
     begin[i] = t[2 * i];
     end[i] = t[2 * i + 1];
   }
-  int khz = 0;
-  HIP_TRY(h, hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, h->device));
-  *ticks_per_s = (int64_t)khz * 1000;
+  *ticks_per_s = h->clock_khz * 1000;
   return BGMF_OK;
 }
 

@@ -33,17 +33,24 @@ __device__ __forceinline__ int64_t gid() {
 
 // ----------------------------------------------------------------- keys
 
+// Key of a rating: (slot - q0, local row).  Every rating's slot lies in
+// [q0, q0 + nq); a slot outside it gets the key nq (past every table) and
+// raises the layout error.
 __global__ void k_make_keys(const int32_t *__restrict__ rows, const int32_t *__restrict__ cols,
-                            int64_t nnz, Grid G, int rbits, uint64_t *__restrict__ keys,
-                            int32_t *__restrict__ idx) {
+                            int64_t nnz, Grid G, int rbits, int64_t q0, int64_t nq,
+                            uint64_t *__restrict__ keys, int32_t *__restrict__ idx, int32_t *err) {
   for (int64_t e = gid(); e < nnz; e += (int64_t)gridDim.x * blockDim.x) {
     const int64_t i = rows[e], j = cols[e];
     const int64_t R = G.row_block(i);
     const int64_t C = G.col_block(j);
     int64_t s = C - R;
     if (s < 0) s += G.p;
-    const uint64_t q = (uint64_t)(s * G.p + R);
-    keys[e] = (q << rbits) | (uint64_t)(i - G.row_start(R));
+    int64_t q = s * G.p + R - q0;
+    if (q < 0 || q >= nq) {
+      atomicOr(err, kErrLayout);
+      q = nq;
+    }
+    keys[e] = ((uint64_t)q << rbits) | (uint64_t)(i - G.row_start(R));
     idx[e] = (int32_t)e;
   }
 }
@@ -248,17 +255,19 @@ __global__ void k_transpose(const int64_t *__restrict__ count, int32_t p,
 
 __global__ void k_gather(const uint64_t *__restrict__ skeys, const int32_t *__restrict__ perm,
                          const int32_t *__restrict__ cols, const float *__restrict__ vals,
-                         int64_t nnz, Grid G, int rbits, const int64_t *__restrict__ block_ptr,
+                         int64_t nnz, Grid G, int rbits, int64_t q0, int64_t nq,
+                         const int64_t *__restrict__ block_ptr,
                          const int64_t *__restrict__ wblock_ptr, bool stratum_major,
                          uint2 *__restrict__ rec, uint8_t *__restrict__ rowrep, int32_t *err) {
   const uint64_t rmask = (rbits == 0) ? 0ull : ((1ull << rbits) - 1ull);
   for (int64_t t = gid(); t < nnz; t += (int64_t)gridDim.x * blockDim.x) {
     const uint64_t key = skeys[t];
-    const int64_t q = (int64_t)(key >> rbits);
-    if (q >= (int64_t)G.p * G.p) {
+    const int64_t ql = (int64_t)(key >> rbits);  // slot relative to q0
+    if (ql >= nq) {
       atomicOr(err, kErrLayout);
       continue;
     }
+    const int64_t q = q0 + ql;
     const uint32_t lrow = (uint32_t)(key & rmask);
     // equal sorted keys = same block and row: the block repeats a row in
     // consecutive ratings (its rows ascend, so equal rows are adjacent)
@@ -272,9 +281,9 @@ __global__ void k_gather(const uint64_t *__restrict__ skeys, const int32_t *__re
     }
     const int32_t j = cols[e];
     const uint32_t lcol = (uint32_t)(j - G.col_start(C));
-    const int64_t beg = block_ptr[q];
+    const int64_t beg = block_ptr[ql];
     const int64_t pos = stratum_major ? t : wblock_ptr[b * G.p + s] + (t - beg);
-    if (pos >= 0 && pos < nnz && t >= beg && t < block_ptr[q + 1])
+    if (pos >= 0 && pos < nnz && t >= beg && t < block_ptr[ql + 1])
       rec[pos] = make_uint2(lrow | (lcol << kColShift), __float_as_uint(vals[e]));
     else
       atomicOr(err, kErrLayout);
@@ -292,28 +301,144 @@ int bits_for(uint64_t values) {  // bits needed to hold 0..values-1
   return b;
 }
 
+// ----------------------------------------------------------------- batched load
+// Pieces of a bucketing that never holds all ratings on the device: slot
+// counts accumulated over batches of the input, and the selection, in input
+// order, of the ratings whose slot lies in a range [q0, q1) (a group of whole
+// blocks, sorted afterwards by bucket() like a load of its own).
+
+__device__ __forceinline__ int64_t slot_of(const Grid &G, int64_t i, int64_t j) {
+  const int64_t R = G.row_block(i);
+  int64_t s = (int64_t)G.col_block(j) - R;
+  if (s < 0) s += G.p;
+  return s * G.p + R;
+}
+
+__global__ void k_slot_count_coo(const int32_t *__restrict__ rows,
+                                 const int32_t *__restrict__ cols, int64_t cnt, Grid G,
+                                 unsigned long long *__restrict__ count) {
+  for (int64_t e = gid(); e < cnt; e += (int64_t)gridDim.x * blockDim.x)
+    atomicAdd(&count[slot_of(G, rows[e], cols[e])], 1ull);
+}
+
+__global__ void k_select_flags(const int32_t *__restrict__ rows, const int32_t *__restrict__ cols,
+                               int64_t cnt, Grid G, int64_t q0, int64_t q1,
+                               int64_t *__restrict__ flag) {
+  for (int64_t e = gid(); e < cnt; e += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t q = slot_of(G, rows[e], cols[e]);
+    flag[e] = (q >= q0 && q < q1) ? 1 : 0;
+  }
+}
+
+// pos[0..cnt]: exclusive prefix of the flags, pos[cnt] the batch total.
+// Selected rating e goes to position *fill + pos[e] of the group arrays, so
+// the group keeps input order; a one-thread kernel then advances *fill by
+// the batch total for the next batch (all on one stream, no host wait).
+__global__ void k_select_compact(const int32_t *__restrict__ rows,
+                                 const int32_t *__restrict__ cols,
+                                 const float *__restrict__ vals, int64_t cnt, int64_t e0, Grid G,
+                                 int64_t q0, int64_t q1, const int64_t *__restrict__ pos,
+                                 const int64_t *__restrict__ fill, int64_t cap,
+                                 int32_t *__restrict__ g_rows, int32_t *__restrict__ g_cols,
+                                 float *__restrict__ g_vals, int32_t *__restrict__ g_e,
+                                 int32_t *err) {
+  const int64_t base = *fill;
+  for (int64_t e = gid(); e < cnt; e += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t q = slot_of(G, rows[e], cols[e]);
+    if (q < q0 || q >= q1) continue;
+    const int64_t d = base + pos[e];
+    if (d < 0 || d >= cap) {
+      atomicOr(err, kErrLayout);
+      continue;
+    }
+    g_rows[d] = rows[e];
+    g_cols[d] = cols[e];
+    g_vals[d] = vals[e];
+    g_e[d] = (int32_t)(e0 + e);
+  }
+}
+
+__global__ void k_advance(int64_t *fill, const int64_t *total) { *fill += *total; }
+
+__global__ void k_map_perm(int32_t *__restrict__ perm, const int32_t *__restrict__ g_e,
+                           int64_t cnt, int32_t *err) {
+  for (int64_t t = gid(); t < cnt; t += (int64_t)gridDim.x * blockDim.x) {
+    const int32_t x = perm[t];
+    if (x < 0 || x >= cnt) {
+      atomicOr(err, kErrLayout);
+      continue;
+    }
+    perm[t] = g_e[x];
+  }
+}
+
 }  // namespace
 
-size_t bucket_scratch_bytes(int64_t nnz, int32_t p) {
+size_t scan_scratch_bytes(int64_t len) {
+  return scan_scratch_count(len) * sizeof(int64_t) + 64 * 256;
+}
+
+hipError_t bucket_count_batch(const int32_t *rows, const int32_t *cols, int64_t cnt,
+                              const Grid &G, int64_t *slot_count, hipStream_t st) {
+  if (cnt <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_slot_count_coo, dim3(grid_for(cnt, kThreads)), dim3(kThreads), 0, st,
+                     rows, cols, cnt, G, reinterpret_cast<unsigned long long *>(slot_count));
+  return hipGetLastError();
+}
+
+hipError_t bucket_offsets(const int64_t *slot_count, int64_t slots, int64_t *block_ptr,
+                          void *scratch, size_t scratch_bytes, hipStream_t st) {
+  Arena ar{static_cast<char *>(scratch), scratch_bytes, 0};
+  return scan_exclusive(slot_count, slots, block_ptr, ar, st);
+}
+
+hipError_t bucket_select_batch(const int32_t *rows, const int32_t *cols, const float *vals,
+                               int64_t cnt, int64_t e0, const Grid &G, int64_t q0, int64_t q1,
+                               int64_t *flag, int64_t *pos, void *scratch, size_t scratch_bytes,
+                               int64_t *fill, const GroupArrays &g, int32_t *err,
+                               hipStream_t st) {
+  if (cnt <= 0) return hipSuccess;
+  const int grid = grid_for(cnt, kThreads);
+  hipLaunchKernelGGL(k_select_flags, dim3(grid), dim3(kThreads), 0, st, rows, cols, cnt, G, q0,
+                     q1, flag);
+  Arena ar{static_cast<char *>(scratch), scratch_bytes, 0};
+  hipError_t e = scan_exclusive(flag, cnt, pos, ar, st);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_select_compact, dim3(grid), dim3(kThreads), 0, st, rows, cols, vals, cnt,
+                     e0, G, q0, q1, pos, fill, g.cap, g.rows, g.cols, g.vals, g.e, err);
+  hipLaunchKernelGGL(k_advance, dim3(1), dim3(1), 0, st, fill, pos + cnt);
+  return hipGetLastError();
+}
+
+hipError_t bucket_map_perm(int32_t *perm, const int32_t *g_e, int64_t cnt, int32_t *err,
+                           hipStream_t st) {
+  if (cnt <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_map_perm, dim3(grid_for(cnt, kThreads)), dim3(kThreads), 0, st, perm, g_e,
+                     cnt, err);
+  return hipGetLastError();
+}
+
+size_t bucket_scratch_bytes(int64_t nnz, int64_t nq) {
   const int64_t tiles = (nnz + kTile - 1) / kTile;
-  const int64_t slots = (int64_t)p * p;
   size_t b = 0;
   b += 2 * (size_t)nnz * sizeof(uint64_t) + 2 * (size_t)nnz * sizeof(int32_t);  // ping-pong
   b += (size_t)kBins * tiles * sizeof(int64_t) * 2;                             // counts, offsets
   b += scan_scratch_count((int64_t)kBins * tiles) * sizeof(int64_t);
-  b += 2 * (size_t)(slots + 1) * sizeof(int64_t);                               // slot counts
-  b += scan_scratch_count(slots) * sizeof(int64_t);
+  b += 2 * (size_t)(nq + 1) * sizeof(int64_t);                                  // slot counts
+  b += scan_scratch_count(nq) * sizeof(int64_t);
   b += 64 * 256;                                                                // alignment
   return b;
 }
 
 hipError_t bucket(const int32_t *rows, const int32_t *cols, const float *vals, int64_t nnz,
-                  const Grid &G, int64_t rows_max, bool stratum_major, void *scratch,
-                  size_t scratch_bytes, const BucketOut &out, int32_t *err, hipStream_t st) {
+                  const Grid &G, int64_t rows_max, int64_t q0, int64_t nq, bool stratum_major,
+                  void *scratch, size_t scratch_bytes, const BucketOut &out, int32_t *err,
+                  hipStream_t st) {
   const int32_t p = G.p;
-  const int64_t slots = (int64_t)p * p;
+  const int64_t slots = nq;
+  if (!stratum_major && (q0 != 0 || nq != (int64_t)p * p)) return hipErrorInvalidValue;
   const int rbits = bits_for((uint64_t)(rows_max < 1 ? 1 : rows_max));
-  const int qbits = bits_for((uint64_t)slots);
+  const int qbits = bits_for((uint64_t)slots + 1);
   const int total_bits = rbits + qbits;
   const int passes = total_bits <= 0 ? 1 : (total_bits + 7) / 8;
   const int64_t tiles = (nnz + kTile - 1) / kTile;
@@ -329,8 +454,8 @@ hipError_t bucket(const int32_t *rows, const int32_t *cols, const float *vals, i
     return hipErrorOutOfMemory;
 
   const int g = grid_for(nnz, kThreads);
-  hipLaunchKernelGGL(k_make_keys, dim3(g), dim3(kThreads), 0, st, rows, cols, nnz, G, rbits, k0,
-                     v0);
+  hipLaunchKernelGGL(k_make_keys, dim3(g), dim3(kThreads), 0, st, rows, cols, nnz, G, rbits, q0,
+                     nq, k0, v0, err);
   uint64_t *kin = k0, *kout = k1;
   int32_t *vin = v0, *vout = v1;
   for (int pass = 0; pass < passes; ++pass) {
@@ -358,9 +483,9 @@ hipError_t bucket(const int32_t *rows, const int32_t *cols, const float *vals, i
     e = scan_exclusive(slot_count, slots, out.block_ptr, scan_ar, st);
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL(k_transpose, dim3(grid_for(slots, kThreads)), dim3(kThreads), 0, st,
-                     slot_count, p, slot_count_w);
-  {
+  if (!stratum_major) {
+    hipLaunchKernelGGL(k_transpose, dim3(grid_for(slots, kThreads)), dim3(kThreads), 0, st,
+                       slot_count, p, slot_count_w);
     Arena scan_ar = ar;
     e = scan_exclusive(slot_count_w, slots, out.wblock_ptr, scan_ar, st);
     if (e != hipSuccess) return e;
@@ -368,8 +493,8 @@ hipError_t bucket(const int32_t *rows, const int32_t *cols, const float *vals, i
   hipLaunchKernelGGL(k_fill_rec, dim3(1), dim3(kThreads), 0, st, out.rec + nnz,
                      (int64_t)kRecPad);
   hipLaunchKernelGGL(k_gather, dim3(g), dim3(kThreads), 0, st, kin, vin, cols, vals, nnz, G,
-                     rbits, out.block_ptr, out.wblock_ptr, stratum_major, out.rec, out.rowrep,
-                     err);
+                     rbits, q0, nq, out.block_ptr, out.wblock_ptr, stratum_major, out.rec,
+                     out.rowrep, err);
   return hipGetLastError();
 }
 

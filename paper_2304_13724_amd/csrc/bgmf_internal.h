@@ -69,7 +69,7 @@ struct SgdParams {
   int32_t cols_max;          // largest column-block width
   int32_t s_begin, s_end;    // strata of this launch
   int64_t g_base;            // global stratum index of stratum 0 of this epoch
-  int64_t wait_ticks;        // wait limit in s_memrealtime ticks (100 MHz)
+  int64_t wait_ticks;        // wait limit in ticks of the constant clock (s_memrealtime)
   float alpha, beta;
   int32_t xcd_remap;
   int32_t passes;            // sweeps of each block before the next (GPU_STEPS >= 1)
@@ -127,11 +127,43 @@ hipError_t rmse_stratum_end(const double *partials, int32_t p, int64_t nnz, doub
 size_t rmse_partials_count(int32_t p);
 // RMSE over caller-given COO ratings already on the device (rows, cols,
 // vals of nnz ratings); partials must hold rmse_coo_partials_count() doubles.
+// *bad is cleared first (by a kernel), then receives bit 1 for a rating
+// outside the n x m matrix and bit 2 for a non-finite value (such ratings
+// are skipped without reading factors).
 constexpr int kRmseCooGroups = 1024;
 size_t rmse_coo_partials_count();
 hipError_t launch_rmse_coo(const int32_t *rows, const int32_t *cols, const float *vals,
-                           int64_t nnz, const float *U, const float *V, int32_t k,
-                           double *partials, double *out, hipStream_t stream);
+                           int64_t nnz, const float *U, const float *V, int32_t k, int64_t n,
+                           int64_t m, double *partials, double *out, int32_t *bad,
+                           hipStream_t stream);
+
+// Batched bucketing (ratings that are never all on the device at once).
+// Slot counts accumulate over batches (slot_count: p*p + 1 int64, zeroed by
+// the caller); bucket_offsets turns them into block_ptr (exclusive prefix,
+// total appended) using scan_scratch_bytes(p*p) of scratch.  A group of
+// whole blocks, slots [q0, q1), is gathered in input order by
+// bucket_select_batch over the same batches (flag and pos: cnt + 1 int64
+// each; fill: device counter of ratings gathered so far, zeroed per group),
+// then sorted by bucket() as a load of its own; bucket_map_perm turns the
+// group-local positions of its perm into input positions.
+struct GroupArrays {
+  int32_t *rows, *cols;
+  float *vals;
+  int32_t *e;   // input position of each gathered rating
+  int64_t cap;  // capacity of each array
+};
+size_t scan_scratch_bytes(int64_t len);
+hipError_t bucket_count_batch(const int32_t *rows, const int32_t *cols, int64_t cnt,
+                              const Grid &G, int64_t *slot_count, hipStream_t stream);
+hipError_t bucket_offsets(const int64_t *slot_count, int64_t slots, int64_t *block_ptr,
+                          void *scratch, size_t scratch_bytes, hipStream_t stream);
+hipError_t bucket_select_batch(const int32_t *rows, const int32_t *cols, const float *vals,
+                               int64_t cnt, int64_t e0, const Grid &G, int64_t q0, int64_t q1,
+                               int64_t *flag, int64_t *pos, void *scratch, size_t scratch_bytes,
+                               int64_t *fill, const GroupArrays &g, int32_t *err,
+                               hipStream_t stream);
+hipError_t bucket_map_perm(int32_t *perm, const int32_t *g_e, int64_t cnt, int32_t *err,
+                           hipStream_t stream);
 
 // Bucketing: from device COO to the block layout.  Scratch buffers are
 // allocated by the caller (see bucket_scratch_bytes).
@@ -143,12 +175,18 @@ struct BucketOut {
   uint8_t *rowrep;      // [p*p] slot q: 1 if two consecutive ratings of the block share a
                         // row (set here; zeroed by the caller)
 };
-size_t bucket_scratch_bytes(int64_t nnz, int32_t p);
-// stratum_major: records in slot order (each stratum contiguous) instead of
-// wave-major order.
+// Scratch of a bucketing of nnz ratings over nq slots.
+size_t bucket_scratch_bytes(int64_t nnz, int64_t nq);
+// Sorts ratings whose slots all lie in [q0, q0 + nq) (any rating outside
+// raises kErrLayout).  out.block_ptr receives nq + 1 offsets relative to
+// slot q0; perm the positions in the given arrays; rowrep is indexed by the
+// global slot.  stratum_major: records in slot order; otherwise (only for
+// the whole grid, q0 = 0 and nq = p*p) records in wave-major order, with
+// out.wblock_ptr.
 // rows_max: the widest row-block (sets the key width).
 hipError_t bucket(const int32_t *rows, const int32_t *cols, const float *vals, int64_t nnz,
-                  const Grid &G, int64_t rows_max, bool stratum_major, void *scratch,
-                  size_t scratch_bytes, const BucketOut &out, int32_t *err, hipStream_t stream);
+                  const Grid &G, int64_t rows_max, int64_t q0, int64_t nq, bool stratum_major,
+                  void *scratch, size_t scratch_bytes, const BucketOut &out, int32_t *err,
+                  hipStream_t stream);
 
 }  // namespace bgmfk

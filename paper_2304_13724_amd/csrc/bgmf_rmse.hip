@@ -207,12 +207,16 @@ k_rmse_stratum(const uint2 *__restrict__ rec, int64_t rec_origin,
 
 // RMSE over caller-given COO ratings (for example a held-out split): the
 // same dot products and fp64 squares, with a lane group per rating taken
-// from a fixed grid-stride order, and one partial per wave.
+// from a fixed grid-stride order, and one partial per wave.  A rating whose
+// row or column lies outside the matrix, or whose value is not finite, adds
+// nothing and sets a bit of *bad (1: index, 2: value); its factor rows are
+// not read.
 template <int KP>
 __global__ void __launch_bounds__(256)
 k_rmse_coo(const int32_t *__restrict__ rows, const int32_t *__restrict__ cols,
            const float *__restrict__ vals, int64_t nnz, const float *__restrict__ U,
-           const float *__restrict__ V, int32_t k, double *__restrict__ partials) {
+           const float *__restrict__ V, int32_t k, int64_t n, int64_t m,
+           double *__restrict__ partials, int32_t *bad) {
   constexpr int L = rmse_lanes<KP>();
   constexpr int RPS = 64 / L;
   constexpr int Q = KP / 4;
@@ -224,10 +228,17 @@ k_rmse_coo(const int32_t *__restrict__ rows, const int32_t *__restrict__ cols,
   const int kq = k / 4;
   double acc = 0.0;
   for (int64_t t = gw * RPS + grp; t - grp < nnz; t += stride) {
-    const bool ok = t < nnz;
+    bool ok = t < nnz;
     const int64_t e = ok ? t : 0;
-    const float4 *up = reinterpret_cast<const float4 *>(U + (int64_t)rows[e] * k);
-    const float4 *vp = reinterpret_cast<const float4 *>(V + (int64_t)cols[e] * k);
+    int64_t i = rows[e], j = cols[e];
+    const float x = vals[e];
+    const bool in = i >= 0 && i < n && j >= 0 && j < m;
+    const bool fin = __builtin_isfinite(x);
+    if (ok && gl == 0 && !(in && fin)) atomicOr(bad, (in ? 0 : 1) | (fin ? 0 : 2));
+    ok = ok && in && fin;
+    if (!in) i = j = 0;
+    const float4 *up = reinterpret_cast<const float4 *>(U + i * k);
+    const float4 *vp = reinterpret_cast<const float4 *>(V + j * k);
     float part = 0.0f;
 #pragma unroll
     for (int i = 0; i < QL; ++i) {
@@ -244,12 +255,14 @@ k_rmse_coo(const int32_t *__restrict__ rows, const int32_t *__restrict__ cols,
     if constexpr (L > 2) part += dpp_mov<0x4E>(part);
     if constexpr (L > 4) part += dpp_mov<0x141>(part);
     if constexpr (L > 8) part += dpp_mov<0x140>(part);
-    const float d = (ok && gl == 0) ? vals[e] - part : 0.0f;
+    const float d = (ok && gl == 0) ? x - part : 0.0f;
     acc = fma((double)d, (double)d, acc);
   }
   for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
   if (lane == 0) partials[gw] = acc;
 }
+
+__global__ void k_zero_i32(int32_t *x) { *x = 0; }
 
 __global__ void k_zero(double *x, int64_t count) {
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count;
@@ -481,14 +494,16 @@ hipError_t rmse_stratum_end(const double *partials, int32_t p, int64_t nnz, doub
 size_t rmse_coo_partials_count() { return (size_t)kRmseCooGroups * kWavesPerGroup; }
 
 hipError_t launch_rmse_coo(const int32_t *rows, const int32_t *cols, const float *vals,
-                           int64_t nnz, const float *U, const float *V, int32_t k,
-                           double *partials, double *out, hipStream_t stream) {
+                           int64_t nnz, const float *U, const float *V, int32_t k, int64_t n,
+                           int64_t m, double *partials, double *out, int32_t *bad,
+                           hipStream_t stream) {
   int kp = 16;
   while (kp < k) kp <<= 1;
   const dim3 grid(kRmseCooGroups), block(64 * kWavesPerGroup);
+  hipLaunchKernelGGL(k_zero_i32, dim3(1), dim3(1), 0, stream, bad);
 #define BGMF_RC(KPV)                                                                           \
   hipLaunchKernelGGL(k_rmse_coo<KPV>, grid, block, 0, stream, rows, cols, vals, nnz, U, V, k, \
-                     partials)
+                     n, m, partials, bad)
   switch (kp) {
     case 16: BGMF_RC(16); break;
     case 32: BGMF_RC(32); break;

@@ -7,6 +7,13 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
+# Load the library before any test imports torch, so that the process's one
+# HIP runtime is the ROCm installation's (see paper_2304_13724_amd/build.py).
+try:
+    import paper_2304_13724_amd.bgmf  # noqa: F401
+except ImportError:
+    pass
+
 
 def pytest_configure(config):
     config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU; run with -m gpu")

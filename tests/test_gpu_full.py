@@ -116,14 +116,38 @@ def test_large_balanced_blocks_one_epoch(large):
 
 
 def test_medium_three_epochs():
+    """The 10M workload: bucketing bit-exact; U, V within 1e-4 of the oracle
+    after the first epoch (the benchmark spec's factor bar); RMSE within 1e-4
+    after each of three epochs; U, V after the third within 3e-4.  The
+    factor bound grows with the epochs because the two sides round the dot
+    products in different orders and every later update starts from the
+    other side's rounded factors: the gap compounds along the dependency
+    chains of the heavy items, while the RMSE, an average over all ratings,
+    stays within 1e-4."""
+    from paper_2304_13724_amd import bgmf
     w = make_config("medium", cache_dir=CACHE)
-    g = _gpu(w, 3)
-    o = _oracle(w, 3)
-    assert np.array_equal(g[0], o[0]) and np.array_equal(g[1], o[1])
-    for a, b in zip(g[4], o[4]):
+    bp_o, perm_o = oracle.bucket(w.n, w.m, w.p, w.rows, w.cols)
+    Uo, Vo = w.U0.copy(), w.V0.copy()
+    hist_o, hist_g = [], []
+    with bgmf.Model(w.n, w.m, w.k, w.p) as mdl:
+        mdl.set_factors(w.U0, w.V0)
+        mdl.load_coo(w.rows, w.cols, w.vals)
+        bp, perm = mdl.get_layout()
+        assert np.array_equal(bp, bp_o) and np.array_equal(perm, perm_o)
+        for e in range(3):
+            mdl.epoch(w.alpha, w.beta)
+            hist_g.append(mdl.rmse())
+            oracle.epoch_mt(w.p, w.rows, w.cols, w.vals, bp_o, perm_o, Uo, Vo, w.alpha, w.beta,
+                            THREADS)
+            hist_o.append(oracle.rmse(w.rows, w.cols, w.vals, Uo, Vo))
+            U, V = mdl.get_factors()
+            du, dv = row_rel_err(U, Uo), row_rel_err(V, Vo)
+            print(f"epoch {e + 1}: row rel err U {du:.3e} V {dv:.3e}, rmse gpu {hist_g[-1]:.9f} "
+                  f"oracle {hist_o[-1]:.9f}", flush=True)
+            bound = TOL if e == 0 else 3 * TOL
+            assert du <= bound and dv <= bound
+    for a, b in zip(hist_g, hist_o):
         assert abs(a - b) <= TOL * b
-    assert row_rel_err(g[2], o[2]) <= 3 * TOL
-    assert row_rel_err(g[3], o[3]) <= 3 * TOL
 
 
 VLARGE_ALPHA = 5e-4  # also the workload's own step (its stated 0.002 diverges)

@@ -158,20 +158,31 @@ def test_errors_and_states():
 
 
 def test_wait_limit_error_path():
-    """A zero wait limit makes any wait that is not satisfied at once give
-    up; the kernel still exits, the error is reported, and the handle keeps
-    working afterwards."""
+    """A zero wait limit on a schedule that is sure to wait: with p = 2,
+    row-block 1's block of stratum 0 holds 200,000 ratings and row-block 0's
+    none, so in stratum 1 wave 0 needs the column-block that wave 1 is still
+    sweeping (some 10 ms), and its first poll finds it unfinished.  The wait
+    gives up, the kernel still exits, the error is reported as
+    BGMF_E_TIMEOUT, and the handle keeps working afterwards."""
     from paper_2304_13724_amd import bgmf
-    w = CASES["medium_shape"]()
+    from workloads.synth import Workload, init_factors
+    rng = np.random.default_rng(11)
+    n = m = 128
+    heavy = 200_000
+    rows = np.r_[rng.integers(64, 128, heavy), rng.integers(0, 64, 100)].astype(np.int32)
+    cols = np.r_[rng.integers(64, 128, heavy), rng.integers(64, 128, 100)].astype(np.int32)
+    vals = rng.integers(1, 6, heavy + 100).astype(np.float32)
+    U0, V0 = init_factors(n, m, 16, 5)
+    w = Workload("wait", n, m, 16, 2, 0.002, 0.05, 1, rows, cols, vals, U0, V0)
     with bgmf.Model(w.n, w.m, w.k, w.p) as mdl:
         mdl.set_factors(w.U0, w.V0)
         mdl.load_coo(w.rows, w.cols, w.vals)
+        assert mdl.get_option(bgmf.BGMF_OPT_PLACEMENT) & 4  # one persistent launch
         mdl.set_option(bgmf.BGMF_OPT_WAIT_LIMIT_US, 0)
         mdl.epoch(w.alpha, w.beta)
-        try:
+        with pytest.raises(bgmf.BgmfError) as ei:
             mdl.sync()
-        except bgmf.BgmfError as e:
-            assert e.code == bgmf.BGMF_E_TIMEOUT
+        assert ei.value.code == bgmf.BGMF_E_TIMEOUT
         mdl.set_option(bgmf.BGMF_OPT_WAIT_LIMIT_US, 10_000_000)
         mdl.set_factors(w.U0, w.V0)
         mdl.epoch(w.alpha, w.beta)
