@@ -200,6 +200,27 @@ int bgmf_balanced_cuts(int64_t n, int64_t m, int32_t p, const int32_t *rows, con
 int bgmf_rmse_coo(bgmf_t *h, const int32_t *rows, const int32_t *cols, const float *vals,
                   int64_t nnz, double *out);
 
+/* bgmf_rmse_coo for callers that cannot allocate memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same RMSE, from the same kernel with the same fixed reduction order
+ * (so the same bits), over nnz ratings already in device memory:
+ *   rows_dev, cols_dev: int32 device arrays, vals_dev: fp32 device array,
+ *   nnz entries each, owned by the caller and read during the call;
+ *   out: host double receiving the RMSE.
+ * It allocates nothing: the reduction's partial sums, its result and an
+ * error word live in a static device array of (4096 + 2) * 8 = 32,784
+ * bytes, one per GPU, held until the process ends.  Every call on a GPU
+ * shares that GPU's array, so calls that overlap on one GPU (other
+ * threads, other handles, other streams) race and their results are
+ * undefined; serialise them.  nnz outside [1, 2^31) -> BGMF_E_ARG (the
+ * largest input the array's fixed-grid reduction serves); needs factors
+ * (BGMF_E_STATE).  Indices and values are checked on the device: a rating
+ * outside the matrix -> BGMF_E_RANGE, a non-finite value ->
+ * BGMF_E_NONFINITE (such ratings are never used to read factors), and
+ * *out is not written.  Waits for the handle's stream. */
+int bgmf_rmse_coo_dev(bgmf_t *h, const int32_t *rows_dev, const int32_t *cols_dev,
+                      const float *vals_dev, int64_t nnz, double *out);
+
 /* Algorithm 1's outer loop (CPU_STEPS = max_epochs, termination deviation
  * delta): RMSE of the initial factors, then up to max_epochs times one epoch
  * and its RMSE pass, stopping after the first epoch whose RMSE differs from

@@ -49,6 +49,7 @@ EXPORTED = (
     "bgmf_sync", "bgmf_factor_ptrs", "bgmf_set_option", "bgmf_get_option", "bgmf_get_timing",
     "bgmf_chain_stats", "bgmf_rmse_coo", "bgmf_fit", "bgmf_set_cuts", "bgmf_get_cuts",
     "bgmf_balanced_cuts", "bgmf_get_trace", "bgmf_query_sizes", "bgmf_bind",
+    "bgmf_rmse_coo_dev",
 )
 
 
@@ -85,6 +86,7 @@ def _load() -> ctypes.CDLL:
         "bgmf_chain_stats": ([vp, vp], c_int),
         "bgmf_get_trace": ([vp, vp, vp, ctypes.POINTER(I64)], c_int),
         "bgmf_rmse_coo": ([vp, vp, vp, vp, I64, ctypes.POINTER(ctypes.c_double)], c_int),
+        "bgmf_rmse_coo_dev": ([vp, vp, vp, vp, I64, ctypes.POINTER(ctypes.c_double)], c_int),
         "bgmf_fit": ([vp, F32, F32, I32, ctypes.c_double, ctypes.POINTER(I32), vp], c_int),
         "bgmf_set_cuts": ([vp, vp, vp], c_int),
         "bgmf_get_cuts": ([vp, vp, vp], c_int),
@@ -248,6 +250,16 @@ def bgmf_rmse_coo(h, rows, cols, vals) -> float:
     out = ctypes.c_double(math.nan)
     _check(h, _lib.bgmf_rmse_coo(h, _ptr(rows), _ptr(cols), _ptr(vals), rows.shape[0],
                                  ctypes.byref(out)))
+    return out.value
+
+
+def bgmf_rmse_coo_dev(h, rows_dev: int, cols_dev: int, vals_dev: int, nnz: int) -> float:
+    """Device addresses as integers (for example ``tensor.data_ptr()``)."""
+    out = ctypes.c_double(math.nan)
+    _check(h, _lib.bgmf_rmse_coo_dev(h, ctypes.c_void_p(int(rows_dev)),
+                                     ctypes.c_void_p(int(cols_dev)),
+                                     ctypes.c_void_p(int(vals_dev)), int(nnz),
+                                     ctypes.byref(out)))
     return out.value
 
 
