@@ -65,8 +65,13 @@ def parse():
     ap.add_argument("--v-staging", type=int, default=0,
                     help="0 automatic, 1 V slice in LDS, 2 V in global memory")
     ap.add_argument("--xcd-remap", type=int, default=1)
-    ap.add_argument("--cpu-seconds", type=float, default=15.0,
-                    help="target CPU time of the oracle baseline sample (0 disables it)")
+    ap.add_argument("--cpu", type=int, default=1, choices=(0, 1),
+                    help="time the CPU oracle on one whole epoch of the workload, "
+                         "multithreaded (the cpu_baseline object; 0 disables it)")
+    ap.add_argument("--cpu-one-thread", type=int, default=1, choices=(0, 1),
+                    help="also time that epoch on one thread")
+    ap.add_argument("--cpu-seconds", type=float, default=None,
+                    help="0 is the same as --cpu 0 (kept for older profile commands)")
     ap.add_argument("--cache", default=os.environ.get("BGMF_WORKLOAD_CACHE", "/tmp/bgmf_cache"))
     ap.add_argument("--traffic", default=TRAFFIC_JSON,
                     help="JSON with measured HBM bytes per sweep launch (ignored if the sweep "
@@ -77,7 +82,10 @@ def parse():
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="run one plain device copy of this size before the timed region (a "
                          "known-size reference for hardware byte counters)")
-    return ap.parse_args()
+    args = ap.parse_args()
+    if args.cpu_seconds == 0:
+        args.cpu = 0
+    return args
 
 
 def log(*a):
@@ -162,54 +170,63 @@ def pmc_l2(csv_path):
     return out
 
 
-def cpu_baseline(w, budget_s, threads=None, layout=None):
-    """Time the CPU oracle (its blocked epoch, multithreaded or on one
-    thread) on the first strata of the same workload, about budget_s seconds
-    of work.  Returns (result, layout)."""
-    import numpy as np
+def host_info():
+    """CPU model, logical CPUs (all, and usable by this process) and RAM of
+    the host, from /proc."""
+    model = None
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    ram_gb = None
+    try:
+        for line in open("/proc/meminfo"):
+            if line.startswith("MemTotal:"):
+                ram_gb = round(int(line.split()[1]) / 1024 ** 2, 1)
+                break
+    except OSError:
+        pass
+    usable = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else None
+    return {"cpu_model": model, "os_cpu_count": os.cpu_count(), "usable_cpus": usable,
+            "ram_gb": ram_gb}
 
+
+# Threads of the multithreaded oracle: one per usable host CPU, at most 16,
+# the host share that goes with one GPU on the benchmark machines.
+CPU_THREADS_MAX = 16
+
+
+def cpu_baseline(w, threads=None, layout=None):
+    """Time the CPU oracle on one whole epoch of the same workload (its
+    blocked epoch: every stratum, every block), multithreaded or on one
+    thread.  Returns (result, layout)."""
     import oracle
 
-    threads = threads or min(16, os.cpu_count() or 1)
+    info = host_info()
+    usable = info["usable_cpus"] or os.cpu_count() or 1
+    threads = threads or min(CPU_THREADS_MAX, usable)
     t0 = time.perf_counter()
     bp, perm = layout if layout is not None else oracle.bucket(w.n, w.m, w.p, w.rows, w.cols)
     t_bucket = time.perf_counter() - t0
-    p = w.p
     U, V = w.U0.copy(), w.V0.copy()
-
-    def run_strata(s0, s1):
-        sub = np.empty_like(bp)
-        lo, hi = s0 * p, s1 * p
-        sub[: lo + 1] = bp[lo]
-        sub[lo: hi + 1] = bp[lo: hi + 1]
-        sub[hi:] = bp[hi]
-        t = time.perf_counter()
-        used = oracle.epoch_mt(p, w.rows, w.cols, w.vals, sub, perm, U, V, w.alpha, w.beta, threads)
-        return time.perf_counter() - t, int(bp[hi] - bp[lo]), used
-
-    # run strata in order (wrapping into further epochs) until the time
-    # budget is used up
-    s0, done, spent, used = 0, 0, 0.0, threads
-    chunk = max(1, min(p, 16))
-    while spent < budget_s:
-        s1 = min(p, s0 + chunk)
-        dt, cnt, used = run_strata(s0, s1)
-        spent += dt
-        done += cnt
-        s0 = 0 if s1 == p else s1
-    dt, cnt = spent, done
-    return {
-        "value": cnt / dt,
+    t = time.perf_counter()
+    used = oracle.epoch_mt(w.p, w.rows, w.cols, w.vals, bp, perm, U, V, w.alpha, w.beta, threads)
+    dt = time.perf_counter() - t
+    res = {
+        "value": w.nnz / dt,
         "unit": "updates/s",
         "cores": used,
         "kind": "oracle",
-        "sample": (f"oracle blocked epoch (C, fp32, {used} threads splitting each stratum's "
-                   f"blocks, strata in order from stratum 0) on the same workload: {cnt} rating "
-                   f"updates in {dt:.2f} s; oracle bucketing of all {w.nnz} ratings took "
-                   f"{t_bucket:.1f} s (untimed)"),
-        "updates": cnt,
-        "seconds": dt,
-    }, (bp, perm)
+        "sample": (f"one whole epoch of the oracle's blocked SGD (C, fp32, {used} threads "
+                   f"splitting each stratum's blocks) over all {w.nnz} ratings of the same "
+                   f"workload: {dt:.2f} s; the oracle's bucketing ({t_bucket:.1f} s) untimed"),
+        "epoch_s": dt,
+    }
+    res.update(info)
+    return res, (bp, perm)
 
 
 def chain_model(stream):
@@ -384,6 +401,42 @@ def main():
             "max_col_block": vchain[0], "max_row_block": vchain[1],
         }
         log(f"balanced blocks: sweep {v_sweep:.2f} ms, step {v_step:.2f} ms")
+    reordered = None
+    if args.variant_steps > 0 and args.balanced_cuts == 0:
+        # the paper's equal blocks on data re-ordered by degree (heavy items
+        # and users spread over the blocks; the other extension Section 3
+        # names): a separate measurement, never `value`
+        rn, cn = bgmf.bgmf_reorder_ids(w.n, w.m, w.p, w.rows, w.cols)
+        U0 = np.empty_like(w.U0)
+        V0 = np.empty_like(w.V0)
+        U0[rn] = w.U0
+        V0[cn] = w.V0
+        rows_r, cols_r = rn[w.rows], cn[w.cols]
+        with bgmf.Model(w.n, w.m, w.k, w.p) as rm:
+            rm.set_stream(stream.cuda_stream)
+            rm.set_factors(U0, V0)
+            rm.load_coo(rows_r, cols_r, w.vals)
+            rchain = [int(x) for x in rm.chain_stats()]
+            rm.epoch(w.alpha, w.beta)
+            rm.rmse()
+            rs = []
+            for _ in range(args.variant_steps):
+                rm.epoch(w.alpha, w.beta)
+                rm.rmse()
+                rs.append(rm.timing())
+        del rows_r, cols_r, U0, V0
+        r_sweep = float(np.mean([x[0] for x in rs]))
+        r_step = float(np.mean([x[0] + x[1] for x in rs]))
+        reordered = {
+            "blocks": "the paper's equal blocks; user and item ids relabelled by degree "
+                      "(bgmf_reorder_ids: heaviest first, each to the least-loaded block with "
+                      "room)",
+            "value": upd / (r_step / 1e3), "unit": "updates/s", "ms_per_step": r_step,
+            "sweep_ms": r_sweep, "roofline_frac": upd * b_alg / (r_sweep / 1e3) / 1e9 / HBM_PEAK_GBS,
+            "max_col_block": rchain[0], "max_row_block": rchain[1],
+            "sum_stratum_max": rchain[2],
+        }
+        log(f"reordered ids: sweep {r_sweep:.2f} ms, step {r_step:.2f} ms, chain {rchain}")
     trace_summary = None
     if args.trace:
         # one more epoch, traced (never part of the timed region)
@@ -399,15 +452,16 @@ def main():
         log(f"trace: {trace_summary}")
     t_dep, copy_gbs = chain_model(stream) if args.model else (None, None)
     cpu = None
-    if args.cpu_seconds > 0:
-        cpu, layout = cpu_baseline(w, args.cpu_seconds)
-        one, _ = cpu_baseline(w, args.cpu_seconds / 2, threads=1, layout=layout)
-        cpu["value_1_thread"] = one["value"]
-        cpu["sample"] += (f"; on one thread (the paper's CMF analogue): {one['updates']} "
-                          f"updates in {one['seconds']:.2f} s")
-        for d in (cpu, one):
-            d.pop("updates")
-            d.pop("seconds")
+    if args.cpu:
+        cpu, layout = cpu_baseline(w)
+        log(f"cpu baseline: {cpu['sample']}")
+        if args.cpu_one_thread:
+            one, _ = cpu_baseline(w, threads=1, layout=layout)
+            cpu["value_1_thread"] = one["value"]
+            cpu["epoch_s_1_thread"] = one["epoch_s"]
+            cpu["sample"] += (f"; the same epoch on one thread (the paper's CMF analogue): "
+                              f"{one['epoch_s']:.2f} s")
+            log(f"cpu baseline, one thread: {one['epoch_s']:.2f} s")
     out = {
         "metric": METRIC,
         "value": value,
@@ -442,6 +496,7 @@ def main():
         },
         "cpu_baseline": cpu,
         "balanced_blocks_variant": variant,
+        "reordered_variant": reordered,
         "sweep_ms": sweep_avg,
         "sweep_ms_median": float(np.median(sweep_ms)),
         "sweep_ms_min": float(np.min(sweep_ms)),

@@ -191,6 +191,22 @@ int bgmf_balanced_cuts(int64_t n, int64_t m, int32_t p, const int32_t *rows, con
                        int64_t nnz, int64_t max_rows, int64_t max_cols, int64_t *row_cuts,
                        int64_t *col_cuts);
 
+/* Data re-ordering (the extension Section 3 names beside variable block
+ * sizes), from host COO arrays (no handle needed): a relabelling of user and
+ * item ids that keeps the paper's equal-dimension blocks (Eq. 4) but spreads
+ * the heavy rows and columns over them.  For each dimension, the indices in
+ * descending number of ratings (ties: ascending index) are dealt one by one
+ * to the block with the smallest number of ratings so far that still has a
+ * free place (ties: lowest block); inside a block, new ids are given in the
+ * order of dealing.  Writes row_newid[i] (n values) and col_newid[j] (m
+ * values), each a permutation; the caller renames its ratings (and initial
+ * factor rows) with them and loads the renamed matrix, on which the method
+ * runs unchanged.  Exact integer arithmetic.  BGMF_E_ARG for p outside
+ * [1, min(n, m)]; BGMF_E_RANGE for a rating outside the matrix.  Errors are
+ * reported by bgmf_last_error(NULL). */
+int bgmf_reorder_ids(int64_t n, int64_t m, int32_t p, const int32_t *rows, const int32_t *cols,
+                     int64_t nnz, int32_t *row_newid, int32_t *col_newid);
+
 /* RMSE of the current factors over nnz caller-given ratings in host COO
  * arrays (for example a held-out split, the paper's Table 2 "test RMSE"):
  * sqrt((1/nnz) sum_e (vals[e] - u_rows[e].v_cols[e])^2), dots in fp32, sum

@@ -49,7 +49,7 @@ EXPORTED = (
     "bgmf_sync", "bgmf_factor_ptrs", "bgmf_set_option", "bgmf_get_option", "bgmf_get_timing",
     "bgmf_chain_stats", "bgmf_rmse_coo", "bgmf_fit", "bgmf_set_cuts", "bgmf_get_cuts",
     "bgmf_balanced_cuts", "bgmf_get_trace", "bgmf_query_sizes", "bgmf_bind",
-    "bgmf_rmse_coo_dev",
+    "bgmf_rmse_coo_dev", "bgmf_reorder_ids",
 )
 
 
@@ -91,6 +91,7 @@ def _load() -> ctypes.CDLL:
         "bgmf_set_cuts": ([vp, vp, vp], c_int),
         "bgmf_get_cuts": ([vp, vp, vp], c_int),
         "bgmf_balanced_cuts": ([I64, I64, I32, vp, vp, I64, I64, I64, vp, vp], c_int),
+        "bgmf_reorder_ids": ([I64, I64, I32, vp, vp, I64, vp, vp], c_int),
         "bgmf_query_sizes": ([vp, I64, ctypes.POINTER(ctypes.c_size_t),
                               ctypes.POINTER(ctypes.c_size_t), ctypes.POINTER(ctypes.c_size_t),
                               ctypes.POINTER(ctypes.c_size_t)], c_int),
@@ -302,6 +303,20 @@ def bgmf_balanced_cuts(n: int, m: int, p: int, rows, cols, max_rows: int = 65536
         msg = _lib.bgmf_last_error(None)
         raise BgmfError(rc, msg.decode() if msg else "bgmf_balanced_cuts failed")
     return r, c
+
+
+def bgmf_reorder_ids(n: int, m: int, p: int, rows, cols):
+    """Returns (row_newid[n], col_newid[m]) as int32 arrays."""
+    rows = np.ascontiguousarray(rows, dtype=np.int32)
+    cols = np.ascontiguousarray(cols, dtype=np.int32)
+    rn = np.empty(int(n), dtype=np.int32)
+    cn = np.empty(int(m), dtype=np.int32)
+    rc = _lib.bgmf_reorder_ids(int(n), int(m), int(p), _ptr(rows), _ptr(cols), rows.shape[0],
+                               _ptr(rn), _ptr(cn))
+    if rc != BGMF_OK:
+        msg = _lib.bgmf_last_error(None)
+        raise BgmfError(rc, msg.decode() if msg else "bgmf_reorder_ids failed")
+    return rn, cn
 
 
 # --- convenience wrapper -----------------------------------------------------

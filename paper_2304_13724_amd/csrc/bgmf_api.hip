@@ -1184,6 +1184,73 @@ int bgmf_balanced_cuts(int64_t n, int64_t m, int32_t p, const int32_t *rows, con
   return BGMF_OK;
 }
 
+namespace {
+
+// Degree-aware relabelling of one dimension over p equal blocks (Eq. 4's
+// boundaries ceil(b len / p)): indices in descending degree (ties by
+// ascending index) are dealt one by one to the block with the smallest load
+// so far that still has a free place (ties by block number); inside a block
+// the new ids follow the order of dealing.  Block widths stay those of the
+// paper's grid, so only the ids change.  newid[old] receives the new id.
+void relabel_dim(const std::vector<int64_t> &deg, int32_t p, int32_t *newid) {
+  const int64_t len = (int64_t)deg.size();
+  std::vector<int64_t> order((size_t)len);
+  for (int64_t i = 0; i < len; ++i) order[i] = i;
+  std::stable_sort(order.begin(), order.end(),
+                   [&](int64_t a, int64_t b) { return deg[a] > deg[b]; });
+  std::vector<int64_t> next((size_t)p), end((size_t)p);
+  for (int32_t b = 0; b < p; ++b) {
+    next[b] = equal_cut(b, len, p);
+    end[b] = equal_cut(b + 1, len, p);
+  }
+  // min-heap of (load, block) over blocks with a free place
+  using Entry = std::pair<int64_t, int32_t>;
+  std::vector<Entry> heap;
+  heap.reserve((size_t)p);
+  for (int32_t b = 0; b < p; ++b)
+    if (next[b] < end[b]) heap.emplace_back(0, b);
+  auto later = [](const Entry &x, const Entry &y) { return x > y; };
+  std::make_heap(heap.begin(), heap.end(), later);
+  for (int64_t i : order) {
+    std::pop_heap(heap.begin(), heap.end(), later);
+    Entry e = heap.back();
+    heap.pop_back();
+    newid[i] = (int32_t)next[e.second]++;
+    if (next[e.second] < end[e.second]) {
+      heap.emplace_back(e.first + deg[i], e.second);
+      std::push_heap(heap.begin(), heap.end(), later);
+    }
+  }
+}
+
+}  // namespace
+
+int bgmf_reorder_ids(int64_t n, int64_t m, int32_t p, const int32_t *rows, const int32_t *cols,
+                     int64_t nnz, int32_t *row_newid, int32_t *col_newid) {
+  if (!rows || !cols || !row_newid || !col_newid || nnz < 0 || n < 1 || m < 1 ||
+      n >= (1ll << 31) || m >= (1ll << 31)) {
+    fail(nullptr, BGMF_E_ARG, "bgmf_reorder_ids: bad arguments");
+    return BGMF_E_ARG;
+  }
+  if (p < 1 || p > n || p > m) {
+    fail(nullptr, BGMF_E_ARG, "bgmf_reorder_ids: p must be in [1, min(n, m)]: p=%d", p);
+    return BGMF_E_ARG;
+  }
+  std::vector<int64_t> rd((size_t)n, 0), cd((size_t)m, 0);
+  for (int64_t e = 0; e < nnz; ++e) {
+    if (rows[e] < 0 || rows[e] >= n || cols[e] < 0 || cols[e] >= m) {
+      fail(nullptr, BGMF_E_RANGE, "rating %lld at (%d, %d) is outside the %lld x %lld matrix",
+           (long long)e, rows[e], cols[e], (long long)n, (long long)m);
+      return BGMF_E_RANGE;
+    }
+    rd[rows[e]] += 1;
+    cd[cols[e]] += 1;
+  }
+  relabel_dim(rd, p, row_newid);
+  relabel_dim(cd, p, col_newid);
+  return BGMF_OK;
+}
+
 int bgmf_set_cuts(bgmf_t *h, const int64_t *row_cuts, const int64_t *col_cuts) {
   if (!h) return BGMF_E_ARG;
   if (!row_cuts || !col_cuts) return fail(h, BGMF_E_ARG, "bgmf_set_cuts: null pointer");

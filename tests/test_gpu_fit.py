@@ -49,7 +49,9 @@ def test_fit_matches_oracle_loop():
         U, V = mdl.get_factors()
     assert ran == len(hist_ref) - 1
     assert np.allclose(hist, hist_ref, rtol=TOL, atol=0)
-    assert row_rel_err(U, U_ref) <= 5 * TOL and row_rel_err(V, V_ref) <= 5 * TOL
+    du, dv = row_rel_err(U, U_ref), row_rel_err(V, V_ref)
+    print(f"fit, {ran} epochs: row rel err U {du:.3e} V {dv:.3e}", flush=True)
+    assert du <= TOL and dv <= TOL
 
 
 def test_heldout_rmse():

@@ -117,13 +117,7 @@ def test_large_balanced_blocks_one_epoch(large):
 
 def test_medium_three_epochs():
     """The 10M workload: bucketing bit-exact; U, V within 1e-4 of the oracle
-    after the first epoch (the benchmark spec's factor bar); RMSE within 1e-4
-    after each of three epochs; U, V after the third within 3e-4.  The
-    factor bound grows with the epochs because the two sides round the dot
-    products in different orders and every later update starts from the
-    other side's rounded factors: the gap compounds along the dependency
-    chains of the heavy items, while the RMSE, an average over all ratings,
-    stays within 1e-4."""
+    after each of three epochs, and the RMSE after each within 1e-4."""
     from paper_2304_13724_amd import bgmf
     w = make_config("medium", cache_dir=CACHE)
     bp_o, perm_o = oracle.bucket(w.n, w.m, w.p, w.rows, w.cols)
@@ -144,8 +138,7 @@ def test_medium_three_epochs():
             du, dv = row_rel_err(U, Uo), row_rel_err(V, Vo)
             print(f"epoch {e + 1}: row rel err U {du:.3e} V {dv:.3e}, rmse gpu {hist_g[-1]:.9f} "
                   f"oracle {hist_o[-1]:.9f}", flush=True)
-            bound = TOL if e == 0 else 3 * TOL
-            assert du <= bound and dv <= bound
+            assert du <= TOL and dv <= TOL
     for a, b in zip(hist_g, hist_o):
         assert abs(a - b) <= TOL * b
 

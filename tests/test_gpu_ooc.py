@@ -96,7 +96,9 @@ def test_ooc_matches_oracle():
     U, V, hist, bp, perm, slots, _, _ = _run(w, 2, budget=2 * _stratum_bytes(w))
     assert slots == 2
     assert np.array_equal(bp, bp_ref) and np.array_equal(perm, perm_ref)
-    assert row_rel_err(U, U_ref) <= 2 * TOL and row_rel_err(V, V_ref) <= 2 * TOL
+    du, dv = row_rel_err(U, U_ref), row_rel_err(V, V_ref)
+    print(f"streamed, 2 epochs: row rel err U {du:.3e} V {dv:.3e}", flush=True)
+    assert du <= TOL and dv <= TOL
     for a, b in zip(hist, hist_ref):
         assert abs(a - b) <= TOL * b
 

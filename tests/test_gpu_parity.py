@@ -86,8 +86,9 @@ def test_tiny_config_all_epochs():
     for a, b in zip(hist, hist_ref):
         assert abs(a - b) <= TOL * b, (hist, hist_ref)
     assert all(y < x for x, y in zip(hist, hist[1:]))
-    assert row_rel_err(U, U_ref) <= 5 * TOL
-    assert row_rel_err(V, V_ref) <= 5 * TOL
+    du, dv = row_rel_err(U, U_ref), row_rel_err(V, V_ref)
+    print(f"tiny, 5 epochs: row rel err U {du:.3e} V {dv:.3e}", flush=True)
+    assert du <= TOL and dv <= TOL
 
 
 def test_xcd_remap_off_matches():

@@ -56,7 +56,9 @@ def _oracle(w, schedule_of_passes):
 
 
 def _close(g, o, tol=TOL):
-    assert row_rel_err(g[0], o[0]) <= tol and row_rel_err(g[1], o[1]) <= tol
+    du, dv = row_rel_err(g[0], o[0]), row_rel_err(g[1], o[1])
+    print(f"row rel err U {du:.3e} V {dv:.3e}", flush=True)
+    assert du <= tol and dv <= tol
     for a, b in zip(g[2], o[2]):
         assert abs(a - b) <= TOL * b
 
@@ -93,7 +95,7 @@ def test_variable_block_iterations():
     w = CASES["medium_shape"]()
     sched = [8, 4, 2, 1]
     o = _oracle(w, sched)
-    _close(_gpu(w, sched), o, tol=3 * TOL)
+    _close(_gpu(w, sched), o, tol=TOL)
 
 
 def test_pass_option_range():
