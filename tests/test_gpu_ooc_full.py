@@ -2,16 +2,18 @@
 k = 64, p = 4096) with the ratings streamed from pinned host memory under a
 16e9-byte device budget.
 
-Opt-in (set BGMF_OOC_FULL=1): it needs about 150 GB of host memory and ten
-minutes, mostly drawing the workload.  At this size the oracle's bucketing
-and epoch are not run (the same shape is checked against the oracle at 50M
-ratings in test_gpu_ooc.py); instead:
+Opt-in (set BGMF_OOC_FULL=1): it needs about 150 GB of host memory and
+some eight minutes (drawing the workload about one, the oracle's bucketing,
+epoch and RMSE most of the rest), more than the default suite may take.
   * the bucketing is checked exactly against its definition: block_ptr is
     the running count of ratings per slot q = s p + R, perm is a
     permutation, and perm lists the ratings in ascending (q, row, input
     position) order, which is the unique stable order the layout promises;
+    and it equals the oracle's bucketing;
   * the streamed epoch is bit-identical to the same epoch with all ratings
-    on the device, and its RMSE is finite and below the initial one.
+    on the device;
+  * U and V after that epoch are within 1e-4 of the oracle's epoch (16
+    threads, bit-identical to its sequential one), and so is the RMSE.
 """
 import os
 import time
@@ -84,12 +86,44 @@ def _check_layout(w, bp, perm):
 
 
 def test_ooc_workload_full():
+    import oracle
+    from helpers import row_rel_err
     w = make_config("ooc", log=_log)
     _log(f"workload drawn: nnz={w.nnz}")
     Us, Vs, r0, r1, bp, perm = _run(w, OOC_BUDGET_BYTES)
     _check_layout(w, bp, perm)
-    del bp, perm
     assert np.isfinite(r1) and r1 < r0
     Ui, Vi, r0i, r1i, _, _ = _run(w, 0)
     assert np.array_equal(Us, Ui) and np.array_equal(Vs, Vi)
     assert abs(r1 - r1i) <= 1e-12 * r1i
+    del Ui, Vi
+    bp_o, perm_o = oracle.bucket(w.n, w.m, w.p, w.rows, w.cols)
+    _log("oracle bucketing done")
+    assert np.array_equal(bp, bp_o) and np.array_equal(perm, perm_o)
+    del bp, perm
+    _log("bucketing equals the oracle's")
+    Uo, Vo = w.U0.copy(), w.V0.copy()
+    oracle.epoch_mt(w.p, w.rows, w.cols, w.vals, bp_o, perm_o, Uo, Vo, w.alpha, w.beta,
+                    min(16, os.cpu_count() or 1))
+    _log("oracle epoch done")
+    du, dv = row_rel_err(Us, Uo), row_rel_err(Vs, Vo)
+    _log(f"row rel err gpu-oracle: U {du:.3e} V {dv:.3e}")
+    assert du <= 1e-4 and dv <= 1e-4
+    # the oracle's RMSE over slices of 1e8 ratings, on the host's threads,
+    # combined as sqrt(sum n_c rmse_c^2 / N) in binary64
+    from concurrent.futures import ThreadPoolExecutor
+    step = 100_000_000
+    spans = [(a, min(a + step, w.nnz)) for a in range(0, w.nnz, step)]
+
+    def part(span):
+        a, b = span
+        return (b - a) * oracle.rmse(w.rows[a:b], w.cols[a:b], w.vals[a:b], Uo, Vo) ** 2
+
+    sq = 0.0
+    with ThreadPoolExecutor(max_workers=min(16, os.cpu_count() or 1)) as ex:
+        for i, v in enumerate(ex.map(part, spans)):
+            sq += v
+            _log(f"oracle rmse: slice {i + 1} of {len(spans)}")
+    ro = float(np.sqrt(sq / w.nnz))
+    _log(f"rmse gpu {r1:.9f} oracle {ro:.9f} rel {abs(r1 - ro) / ro:.3e}")
+    assert abs(r1 - ro) <= 1e-4 * ro
