@@ -335,10 +335,13 @@ int bgmf_factor_ptrs(bgmf_t *h, float **U_dev, float **V_dev);
                                     can vary it from epoch to epoch (the paper's
                                     variable block iterations). */
 #define BGMF_OPT_SINGLE_COLUMN 11 /* 1 (default): with V staged in LDS, a block
-                                    whose column-block is one column wide (a heavy
-                                    item given a column-block of its own through
-                                    bgmf_set_cuts) and whose consecutive ratings
-                                    never share a row keeps that column's v in
+                                    whose ratings all lie on one column (always so
+                                    when its column-block is one column wide, as a
+                                    heavy item given a column-block of its own
+                                    through bgmf_set_cuts; often so for a heavy
+                                    item's blocks after bgmf_reorder_ids) and
+                                    whose consecutive ratings never share a row
+                                    keeps that column's v in
                                     registers from its first rating to its last
                                     and forms each rating's partial products
                                     before the previous error is known (a shorter

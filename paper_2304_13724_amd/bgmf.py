@@ -359,6 +359,20 @@ class Model:
              pinned_bytes: int = 0, stream=None):
         bgmf_bind(self.h, U_dev, V_dev, ws_dev, ws_bytes, pinned_host, pinned_bytes, stream)
 
+    def bind_tensors(self, U, V, ws, pinned=None, stream=None):
+        """bind() with tensors (anything with data_ptr(), numel() and
+        element_size(), such as torch tensors): U (n x k) and V (m x k) float32
+        on the device, ws a device byte buffer, pinned a pinned host byte
+        buffer or None, stream an integer hipStream_t or None."""
+        def nbytes(t):
+            return int(t.numel()) * int(t.element_size())
+        for t, rows in ((U, self.n), (V, self.m)):
+            if nbytes(t) != rows * self.k * 4:
+                raise ValueError("U must hold n x k and V m x k float32 values")
+        bgmf_bind(self.h, U.data_ptr(), V.data_ptr(), ws.data_ptr(), nbytes(ws),
+                  pinned.data_ptr() if pinned is not None else 0,
+                  nbytes(pinned) if pinned is not None else 0, stream)
+
     def load_coo(self, rows, cols, vals):
         bgmf_load_coo(self.h, rows, cols, vals)
         self.nnz = int(np.asarray(rows).shape[0])

@@ -49,7 +49,7 @@ def build(verbose: bool = False) -> str:
     """Compile every HIP source into paper_2304_13724_amd/libbgmf.so."""
     tmp = LIB + ".tmp"
     cmd = [HIPCC, *FLAGS, "-L", _runtime_name_stub(), "-I", os.path.join(ROOT, "include"),
-           *sources(), "-o", tmp]
+           *sources(), "-lrocprofiler-sdk-roctx", "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)

@@ -12,10 +12,25 @@
 #include <string>
 #include <vector>
 
+#include <rocprofiler-sdk-roctx/roctx.h>
+
 #include "../../include/bgmf.h"
 #include "bgmf_handle.h"
 
 using namespace bgmfk;
+
+namespace {
+
+// A named range around each call that does device work, for profilers that
+// record ROCTx markers (rocprofv3 --marker-trace); no cost when none listens.
+struct Range {
+  explicit Range(const char *name) { roctxRangePushA(name); }
+  ~Range() { roctxRangePop(); }
+  Range(const Range &) = delete;
+  Range &operator=(const Range &) = delete;
+};
+
+}  // namespace
 
 namespace {
 
@@ -136,7 +151,7 @@ void free_layout(bgmf_t *h) {
   h->slot_used.clear();
   h->chunk.clear();
   h->block_ptr = h->wblock_ptr = nullptr;
-  h->rowrep = nullptr;
+  h->nofold = nullptr;
   h->perm = nullptr;
   h->rec = h->ring = h->host_rec = h->resident = nullptr;
   h->s_res = 0;
@@ -297,7 +312,7 @@ int load_incore(bgmf_t *h, const int32_t *rows, const int32_t *cols, const float
   }
   h->block_ptr = kc.take<int64_t>(slots + 1);
   h->wblock_ptr = kc.take<int64_t>(slots + 1);
-  h->rowrep = kc.take<uint8_t>(slots);
+  h->nofold = kc.take<uint8_t>(slots);
   h->rec = kc.take<uint2>(nnz + kRecPad);
   h->perm = kc.take<int32_t>(nnz);
   if (h->bound) tc = Carve{h->ws, h->ws_bytes, kc.used, kc.used};
@@ -310,7 +325,7 @@ int load_incore(bgmf_t *h, const int32_t *rows, const int32_t *cols, const float
     if (rc != BGMF_OK) free_layout(h);
     return rc;
   };
-  if (!h->block_ptr || !h->wblock_ptr || !h->rowrep || !h->rec || !h->perm || !d_rows ||
+  if (!h->block_ptr || !h->wblock_ptr || !h->nofold || !h->rec || !h->perm || !d_rows ||
       !d_cols || !d_vals || !scratch)
     return done(fail(h, BGMF_E_HIP, "internal error: in-core load does not fit its plan"));
   h->load_peak = (int64_t)(incore_keep_bytes(nnz) + temp);
@@ -329,8 +344,8 @@ int load_incore(bgmf_t *h, const int32_t *rows, const int32_t *cols, const float
   LOAD_TRY(hipMemcpyAsync(d_vals, vals, (size_t)nnz * sizeof(float), hipMemcpyHostToDevice,
                           h->stream));
   LOAD_TRY(hipMemsetAsync(h->err, 0, sizeof(int32_t), h->stream));
-  LOAD_TRY(hipMemsetAsync(h->rowrep, 0, (size_t)slots, h->stream));
-  BucketOut out{h->block_ptr, h->wblock_ptr, h->perm, h->rec, h->rowrep};
+  LOAD_TRY(hipMemsetAsync(h->nofold, 0, (size_t)slots, h->stream));
+  BucketOut out{h->block_ptr, h->wblock_ptr, h->perm, h->rec, h->nofold};
   LOAD_TRY(bucket(d_rows, d_cols, d_vals, nnz, grid_of(h), h->rows_max, 0, slots, false,
                   scratch, scratch_bytes, out, h->err, h->stream));
   LOAD_TRY(hipStreamSynchronize(h->stream));
@@ -404,9 +419,9 @@ int load_streamed(bgmf_t *h, const int32_t *rows, const int32_t *cols, const flo
     tc = Carve{static_cast<char *>(h->own_persist), tab};
   }
   h->block_ptr = tc.take<int64_t>(slots + 1);
-  h->rowrep = tc.take<uint8_t>(slots);
+  h->nofold = tc.take<uint8_t>(slots);
   h->wblock_ptr = nullptr;
-  if (!h->host_rec || !h->host_perm || !h->block_ptr || !h->rowrep)
+  if (!h->host_rec || !h->host_perm || !h->block_ptr || !h->nofold)
     return bail(BGMF_E_HIP, "internal error: streamed load does not fit its plan");
   // the ratings region: the rest of a bound workspace, or allocated per pass
   const size_t ws_rest = h->bound ? h->ws_bytes - aligned(tc.used) : 0;
@@ -565,7 +580,7 @@ int load_streamed(bgmf_t *h, const int32_t *rows, const int32_t *cols, const flo
       return bail(BGMF_E_HIP, "internal error: group pass does not fit its plan");
     peak = std::max(peak, c.high);
     LOAD_TRY(hipMemsetAsync(h->err, 0, sizeof(int32_t), h->stream));
-    LOAD_TRY(hipMemsetAsync(h->rowrep, 0, (size_t)slots, h->stream));
+    LOAD_TRY(hipMemsetAsync(h->nofold, 0, (size_t)slots, h->stream));
     std::vector<int64_t> got;
     for (const auto &gr : groups) {
       const int64_t q0 = gr.first, q1 = gr.second, gcnt = bp[q1] - bp[q0];
@@ -578,7 +593,7 @@ int load_streamed(bgmf_t *h, const int32_t *rows, const int32_t *cols, const flo
         LOAD_TRY(bucket_select_batch(b_rows, b_cols, b_vals, cnt, e0, G, q0, q1, flag, pos, ss,
                                      ssb, fill, g, h->err, h->stream));
       }
-      BucketOut out{bp_t, nullptr, perm_t, rec_t, h->rowrep};
+      BucketOut out{bp_t, nullptr, perm_t, rec_t, h->nofold};
       LOAD_TRY(bucket(g.rows, g.cols, g.vals, gcnt, G, h->rows_max, q0, q1 - q0, true, bs, bsb,
                       out, h->err, h->stream));
       LOAD_TRY(bucket_map_perm(perm_t, g.e, gcnt, h->err, h->stream));
@@ -857,6 +872,7 @@ int bgmf_bind(bgmf_t *h, float *U_dev, float *V_dev, void *ws_dev, size_t ws_byt
 
 int bgmf_set_factors(bgmf_t *h, const float *U, const float *V) {
   if (!h) return BGMF_E_ARG;
+  const Range range("bgmf_set_factors");
   if (!U || !V) return fail(h, BGMF_E_ARG, "bgmf_set_factors: null pointer");
   for (int64_t x = 0, cnt = h->n * h->k; x < cnt; ++x)
     if (!std::isfinite(U[x])) return fail(h, BGMF_E_NONFINITE, "U[%lld] is not finite", (long long)x);
@@ -874,6 +890,7 @@ int bgmf_set_factors(bgmf_t *h, const float *U, const float *V) {
 int bgmf_load_coo(bgmf_t *h, const int32_t *rows, const int32_t *cols, const float *vals,
                   int64_t nnz) {
   if (!h) return BGMF_E_ARG;
+  const Range range("bgmf_load_coo");
   if (!rows || !cols || !vals) return fail(h, BGMF_E_ARG, "bgmf_load_coo: null pointer");
   if (nnz < 1 || nnz >= (1ll << 31))
     return fail(h, BGMF_E_ARG, "nnz must be in [1, 2^31): %lld", (long long)nnz);
@@ -991,6 +1008,7 @@ SweepShape sweep_shape(const bgmf_t *h) {
 
 int bgmf_epoch(bgmf_t *h, float alpha, float beta) {
   if (!h) return BGMF_E_ARG;
+  const Range range("bgmf_epoch");
   if (!std::isfinite(alpha) || !(alpha > 0.0f) || !std::isfinite(beta) || beta < 0.0f)
     return fail(h, BGMF_E_ARG, "alpha must be finite and > 0, beta finite and >= 0");
   if (!h->loaded) return fail(h, BGMF_E_STATE, "bgmf_epoch: no ratings loaded");
@@ -1019,7 +1037,7 @@ int bgmf_epoch(bgmf_t *h, float alpha, float beta) {
   P.xcd_remap = (int32_t)h->xcd_remap;
   P.passes = (int32_t)h->passes;
   P.single_col = (int32_t)h->single_col;
-  P.rowrep = h->rowrep;
+  P.nofold = h->nofold;
   const SweepShape sh = sweep_shape(h);
   P.lds_ring = sh.lds ? h->lds_ring : 0;
   if (h->d_trace) {
@@ -1084,6 +1102,7 @@ int bgmf_epoch(bgmf_t *h, float alpha, float beta) {
 
 int bgmf_rmse(bgmf_t *h, double *out) {
   if (!h) return BGMF_E_ARG;
+  const Range range("bgmf_rmse");
   if (!out) return fail(h, BGMF_E_ARG, "bgmf_rmse: null output");
   if (!h->loaded) return fail(h, BGMF_E_STATE, "bgmf_rmse: no ratings loaded");
   if (!h->factors_set) return fail(h, BGMF_E_STATE, "bgmf_rmse: factors not set");
@@ -1341,6 +1360,7 @@ int bgmf_rmse_coo(bgmf_t *h, const int32_t *rows, const int32_t *cols, const flo
 int bgmf_fit(bgmf_t *h, float alpha, float beta, int32_t max_epochs, double delta,
              int32_t *epochs_run, double *rmse_history) {
   if (!h) return BGMF_E_ARG;
+  const Range range("bgmf_fit");
   if (!epochs_run) return fail(h, BGMF_E_ARG, "bgmf_fit: null epochs_run");
   if (max_epochs < 1) return fail(h, BGMF_E_ARG, "max_epochs must be >= 1");
   if (!std::isfinite(delta) || delta < 0.0) return fail(h, BGMF_E_ARG, "delta must be finite and >= 0");
@@ -1370,6 +1390,7 @@ int bgmf_fit(bgmf_t *h, float alpha, float beta, int32_t max_epochs, double delt
 
 int bgmf_get_factors(bgmf_t *h, float *U, float *V) {
   if (!h) return BGMF_E_ARG;
+  const Range range("bgmf_get_factors");
   if (U)
     HIP_TRY(h, hipMemcpyAsync(U, h->U, (size_t)h->n * h->k * sizeof(float), hipMemcpyDeviceToHost,
                               h->stream));

@@ -258,7 +258,7 @@ __global__ void k_gather(const uint64_t *__restrict__ skeys, const int32_t *__re
                          int64_t nnz, Grid G, int rbits, int64_t q0, int64_t nq,
                          const int64_t *__restrict__ block_ptr,
                          const int64_t *__restrict__ wblock_ptr, bool stratum_major,
-                         uint2 *__restrict__ rec, uint8_t *__restrict__ rowrep, int32_t *err) {
+                         uint2 *__restrict__ rec, uint8_t *__restrict__ nofold, int32_t *err) {
   const uint64_t rmask = (rbits == 0) ? 0ull : ((1ull << rbits) - 1ull);
   for (int64_t t = gid(); t < nnz; t += (int64_t)gridDim.x * blockDim.x) {
     const uint64_t key = skeys[t];
@@ -269,9 +269,14 @@ __global__ void k_gather(const uint64_t *__restrict__ skeys, const int32_t *__re
     }
     const int64_t q = q0 + ql;
     const uint32_t lrow = (uint32_t)(key & rmask);
-    // equal sorted keys = same block and row: the block repeats a row in
-    // consecutive ratings (its rows ascend, so equal rows are adjacent)
-    if (t > 0 && skeys[t - 1] == key) rowrep[q] = 1;
+    // the folded one-column step needs every rating of the block on one
+    // column and no row twice in a row: equal sorted keys are the same block
+    // and row (rows ascend inside a block, so equal rows are adjacent), and
+    // a column that differs from the previous rating's in the same block
+    // means more than one column
+    if (t > 0 && (skeys[t - 1] >> rbits) == (key >> rbits) &&
+        (skeys[t - 1] == key || cols[perm[t - 1]] != cols[perm[t]]))
+      nofold[q] = 1;
     const int64_t s = q / G.p, b = q - s * G.p;
     const int64_t C = (b + s) % G.p;
     const int32_t e = perm[t];
@@ -494,7 +499,7 @@ hipError_t bucket(const int32_t *rows, const int32_t *cols, const float *vals, i
                      (int64_t)kRecPad);
   hipLaunchKernelGGL(k_gather, dim3(g), dim3(kThreads), 0, st, kin, vin, cols, vals, nnz, G,
                      rbits, q0, nq, out.block_ptr, out.wblock_ptr, stratum_major, out.rec,
-                     out.rowrep, err);
+                     out.nofold, err);
   return hipGetLastError();
 }
 

@@ -23,7 +23,7 @@ struct bgmf {
   // ratings layout
   int64_t nnz = 0;
   int64_t *block_ptr = nullptr, *wblock_ptr = nullptr;
-  uint8_t *rowrep = nullptr;  // [p*p] per block slot: a row repeats in consecutive ratings
+  uint8_t *nofold = nullptr;  // [p*p] per block slot: the folded one-column step does not apply
   int32_t *perm = nullptr;
   uint2 *rec = nullptr;
   int64_t *flags = nullptr;

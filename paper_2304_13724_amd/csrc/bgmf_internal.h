@@ -73,9 +73,10 @@ struct SgdParams {
   float alpha, beta;
   int32_t xcd_remap;
   int32_t passes;            // sweeps of each block before the next (GPU_STEPS >= 1)
-  int32_t single_col;        // 1: blocks of a one-column column-block keep v in registers
-  const uint8_t *rowrep;     // [p * p], slot s*p + b: 1 if two consecutive ratings of the
-                             // block share a row
+  int32_t single_col;        // 1: blocks whose ratings are all on one column keep v in
+                             // registers (the folded one-column step)
+  const uint8_t *nofold;     // [p * p], slot s*p + b: 1 if the block cannot take the folded
+                             // step (a row repeats in consecutive ratings, or two columns)
   int32_t lds_ring;          // LDS sweep, persistent launches: areas in the workgroup's
                              // hand-over ring (0: each wave its own area, global hand-over)
   int64_t *trace;            // null, or [2 p p]: per block slot s*p + b, the clock when the
@@ -172,14 +173,14 @@ struct BucketOut {
   int64_t *wblock_ptr;  // [p*p + 1] wave-major block starts
   int32_t *perm;        // [nnz] input position of each slot-ordered rating
   uint2 *rec;           // [nnz + kRecPad] wave-major records
-  uint8_t *rowrep;      // [p*p] slot q: 1 if two consecutive ratings of the block share a
-                        // row (set here; zeroed by the caller)
+  uint8_t *nofold;      // [p*p] slot q: 1 if two consecutive ratings of the block share a
+                        // row or differ in column (set here; zeroed by the caller)
 };
 // Scratch of a bucketing of nnz ratings over nq slots.
 size_t bucket_scratch_bytes(int64_t nnz, int64_t nq);
 // Sorts ratings whose slots all lie in [q0, q0 + nq) (any rating outside
 // raises kErrLayout).  out.block_ptr receives nq + 1 offsets relative to
-// slot q0; perm the positions in the given arrays; rowrep is indexed by the
+// slot q0; perm the positions in the given arrays; nofold is indexed by the
 // global slot.  stratum_major: records in slot order; otherwise (only for
 // the whole grid, q0 = 0 and nq = p*p) records in wave-major order, with
 // out.wblock_ptr.

@@ -12,9 +12,10 @@
 // Per wave and block:
 //   * V: either the block's column slice (ncols x k fp32) is copied into LDS
 //     after the acquire, updated there and written back before the release
-//     (k_sgd_lds; a slice one column wide instead stays in registers for the
-//     whole block, with a shorter dependency chain per rating when no row
-//     repeats), or V stays in global memory and each rating's v row is
+//     (k_sgd_lds; when all of a block's ratings are on one column, that
+//     column's v instead stays in registers for the whole block, with a
+//     shorter dependency chain per rating when no row repeats), or V stays
+//     in global memory and each rating's v row is
 //     prefetched like the u rows (k_sgd_gv, for slices too wide for LDS);
 //   * U rows are owned by the wave for the whole launch; they are prefetched
 //     from HBM kPrefetch ratings ahead into a register ring and stored after
@@ -377,8 +378,9 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
     const int64_t beg = uniform64(bx[0]);
     const int32_t len = (int32_t)(uniform64(bx[1]) - beg);
     const uint2 *rp = P.rec + (beg - P.rec_origin);
-    const bool fold = ncols == 1 && P.single_col &&
-                      __builtin_amdgcn_readfirstlane(P.rowrep[(int64_t)s * P.p + b]) == 0;
+    // every rating of the block on one column, no row twice in a row
+    const bool fold = P.single_col &&
+                      __builtin_amdgcn_readfirstlane(P.nofold[(int64_t)s * P.p + b]) == 0;
     // this lane's part of the LDS area holding column-block C; whether the
     // slice comes from wave w + 1 of this workgroup (through LDS) and goes
     // on to wave w - 1 (through LDS)
@@ -595,9 +597,10 @@ __global__ void __launch_bounds__(256) k_sgd_lds(SgdParams P) {
         Wn1 = Wn2;
       };
 
-      // Folded step of a one-column block in which no row repeats in
-      // consecutive ratings (every block of a heavy item's own
-      // column-block, with cut points of unequal blocks).  The next rating
+      // Folded step of a block whose ratings all lie on one column and in
+      // which no row repeats in consecutive ratings (every block of a heavy
+      // item's own column-block, with cut points of unequal blocks, and most
+      // blocks of a heavy item's column-block after re-ordering).  The next rating
       // has another row u' and the same column, so its partial products are
       //   x'/KPL - u'.(v + d_v + (a e) u) = [x'/KPL - u'.(v + d_v)] - e [u'.(a u)]
       // with d_v = -(a b) v: both brackets are known before e, and the

@@ -30,16 +30,19 @@ def oracle_run(w, epochs, threads=1, layout=None):
     return U, V, hist, bp, perm
 
 
-def gpu_run(w, epochs, schedule=0, xcd_remap=1, v_staging=0, budget=0):
+def gpu_run(w, epochs, schedule=0, xcd_remap=1, v_staging=0, budget=0, single=1):
     """Run the HIP path through the C ABI; returns (U, V, rmse_history, block_ptr, perm).
     ``v_staging``: 0 automatic, 1 V slice in LDS, 2 V in global memory;
-    ``budget``: ratings budget in bytes (0 = all ratings on the device)."""
+    ``budget``: ratings budget in bytes (0 = all ratings on the device);
+    ``single``: BGMF_OPT_SINGLE_COLUMN (0 when a run with V in LDS is compared
+    bit for bit with one with V in global memory, which has no folded step)."""
     from paper_2304_13724_amd import bgmf
     with bgmf.Model(w.n, w.m, w.k, w.p) as mdl:
         mdl.set_option(bgmf.BGMF_OPT_SCHEDULE, schedule)
         mdl.set_option(bgmf.BGMF_OPT_XCD_REMAP, xcd_remap)
         mdl.set_option(bgmf.BGMF_OPT_V_STAGING, v_staging)
         mdl.set_option(bgmf.BGMF_OPT_RATINGS_BUDGET, budget)
+        mdl.set_option(bgmf.BGMF_OPT_SINGLE_COLUMN, single)
         mdl.set_factors(w.U0, w.V0)
         mdl.load_coo(w.rows, w.cols, w.vals)
         bp, perm = mdl.get_layout()

@@ -54,9 +54,7 @@ def _bound(w, epochs, ws_bytes=None, pinned=True, budget=0):
                  if pinned else None)
         torch.cuda.synchronize()
         mdl.set_option(bgmf.BGMF_OPT_RATINGS_BUDGET, budget)
-        mdl.bind(U_t.data_ptr(), V_t.data_ptr(), ws_t.data_ptr(), ws_bytes,
-                 pin_t.data_ptr() if pinned else 0, sizes["pinned_bytes"] if pinned else 0,
-                 stream.cuda_stream)
+        mdl.bind_tensors(U_t, V_t, ws_t, pin_t, stream.cuda_stream)
         before = mdl.get_option(bgmf.BGMF_OPT_ALLOC_COUNT)
         mdl.load_coo(w.rows, w.cols, w.vals)
         hist = []

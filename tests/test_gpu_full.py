@@ -154,6 +154,7 @@ def test_vlarge_one_epoch_parity():
     print(f"gpu rmse {g[4]}", flush=True)
     with bgmf.Model(w.n, w.m, w.k, w.p) as mdl:  # the same epoch with V staged in LDS
         mdl.set_option(bgmf.BGMF_OPT_V_STAGING, 1)
+        mdl.set_option(bgmf.BGMF_OPT_SINGLE_COLUMN, 0)  # the global-V sweep has no fold
         mdl.set_factors(w.U0, w.V0)
         mdl.load_coo(w.rows, w.cols, w.vals)
         mdl.epoch(w.alpha, w.beta)

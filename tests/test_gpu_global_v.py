@@ -57,7 +57,7 @@ CASES = {
 @pytest.mark.parametrize("schedule", [0, 1, 2])
 def test_bit_identical_to_lds(case, schedule):
     w = CASES[case]()
-    a = gpu_run(w, 2, schedule=schedule, v_staging=LDS)
+    a = gpu_run(w, 2, schedule=schedule, v_staging=LDS, single=0)
     g = gpu_run(w, 2, schedule=schedule, v_staging=GLOBAL)
     assert np.array_equal(g[0], a[0]) and np.array_equal(g[1], a[1])
     assert g[2] == a[2]
@@ -119,7 +119,7 @@ def test_handover_stress(k, p):
              epochs=3, seed=p + k + 1, structure="uniform", values="int5", rank=4)
     a = gpu_run(w, 3, v_staging=GLOBAL, schedule=2)
     b = gpu_run(w, 3, v_staging=GLOBAL, schedule=2)
-    c = gpu_run(w, 3, v_staging=LDS)
+    c = gpu_run(w, 3, v_staging=LDS, single=0)
     assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
     assert np.array_equal(a[0], c[0]) and np.array_equal(a[1], c[1])
 
@@ -131,7 +131,7 @@ def test_out_of_core_global_v():
     bp, _ = oracle.bucket(w.n, w.m, w.p, w.rows, w.cols)
     budget = 3 * (int(np.diff(bp[:: w.p]).max()) + 256) * 8
     a = gpu_run(w, 2, v_staging=GLOBAL, budget=budget)
-    b = gpu_run(w, 2, v_staging=LDS)
+    b = gpu_run(w, 2, v_staging=LDS, single=0)
     assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
     # the streamed RMSE pass adds its fp64 partial sums in another grouping
     for x, y in zip(a[2], b[2]):

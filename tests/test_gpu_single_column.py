@@ -198,3 +198,40 @@ def test_fold_correction_term_is_exercised():
     assert ratio > 0.05
     o = _oracle(w, rc, cc)
     _check_oracle(_gpu(w, rc, cc, 1), o)
+
+
+def test_one_distinct_column_in_wider_blocks():
+    """The paper's equal blocks (16 columns wide), where every block of
+    column-block 0 has all its ratings on column 5 (each user rates it once)
+    and the other column-blocks are ordinary: those blocks take the folded
+    step although their column-block is wider than one column (the option
+    then changes the last bits of column 5, which shows the fold ran), and one epoch
+    matches the oracle within the tolerance either way."""
+    from paper_2304_13724_amd import bgmf
+    n, m, p, k = 2_000, 64, 4, 64
+    rng = np.random.default_rng(23)
+    rows = np.r_[np.arange(n), rng.integers(0, n, 20_000)].astype(np.int32)
+    cols = np.r_[np.full(n, 5), rng.integers(16, m, 20_000)].astype(np.int32)
+    order = rng.permutation(len(rows))
+    w = _W()
+    w.n, w.m, w.k, w.p = n, m, k, p
+    w.rows, w.cols = rows[order], cols[order]
+    w.vals = rng.integers(1, 6, len(rows)).astype(np.float32)
+    w.U0, w.V0 = init_factors(n, m, k, 3)
+    w.alpha, w.beta = 0.01, 0.05
+    bp, perm = oracle.bucket(n, m, p, w.rows, w.cols)
+    Uo, Vo = w.U0.copy(), w.V0.copy()
+    oracle.epoch(p, w.rows, w.cols, w.vals, bp, perm, Uo, Vo, w.alpha, w.beta)
+    out = {}
+    for single in (1, 0):
+        with bgmf.Model(n, m, k, p) as mdl:
+            mdl.set_option(bgmf.BGMF_OPT_SINGLE_COLUMN, single)
+            mdl.set_factors(w.U0, w.V0)
+            mdl.load_coo(w.rows, w.cols, w.vals)
+            assert mdl.get_option(bgmf.BGMF_OPT_PLACEMENT) & 1  # V staged in LDS
+            mdl.epoch(w.alpha, w.beta)
+            out[single] = mdl.get_factors()
+        du, dv = row_rel_err(out[single][0], Uo), row_rel_err(out[single][1], Vo)
+        print(f"single_column={single}: row rel err U {du:.3e} V {dv:.3e}", flush=True)
+        assert du <= TOL and dv <= TOL
+    assert not np.array_equal(out[1][1][5], out[0][1][5])  # column 5 went through the fold
