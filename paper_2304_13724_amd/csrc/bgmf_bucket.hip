@@ -260,7 +260,27 @@ __global__ void k_gather(const uint64_t *__restrict__ skeys, const int32_t *__re
                          const int64_t *__restrict__ wblock_ptr, bool stratum_major,
                          uint2 *__restrict__ rec, uint8_t *__restrict__ nofold, int32_t *err) {
   const uint64_t rmask = (rbits == 0) ? 0ull : ((1ull << rbits) - 1ull);
-  for (int64_t t = gid(); t < nnz; t += (int64_t)gridDim.x * blockDim.x) {
+  const int lane = threadIdx.x & 63;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  // t0 is the same for the 64 lanes of a wave (lane l takes t0 + l), so the
+  // previous rating's column comes from the lane before (one read per wave
+  // for lane 0) instead of a second random read of the input
+  for (int64_t t0 = gid() - lane; t0 < nnz; t0 += stride) {
+    const int64_t t = t0 + lane;
+    const bool in = t < nnz;
+    const int32_t e = in ? perm[t] : 0;
+    const bool e_ok = in && e >= 0 && e < nnz;
+    const int32_t j = e_ok ? cols[e] : -1;
+    int32_t jprev = __shfl_up(j, 1);
+    if (lane == 0 && in && t > 0) {
+      const int32_t ep = perm[t - 1];
+      jprev = (ep >= 0 && ep < nnz) ? cols[ep] : -1;
+    }
+    if (!in) continue;
+    if (!e_ok) {
+      atomicOr(err, kErrLayout);
+      continue;
+    }
     const uint64_t key = skeys[t];
     const int64_t ql = (int64_t)(key >> rbits);  // slot relative to q0
     if (ql >= nq) {
@@ -275,16 +295,10 @@ __global__ void k_gather(const uint64_t *__restrict__ skeys, const int32_t *__re
     // a column that differs from the previous rating's in the same block
     // means more than one column
     if (t > 0 && (skeys[t - 1] >> rbits) == (key >> rbits) &&
-        (skeys[t - 1] == key || cols[perm[t - 1]] != cols[perm[t]]))
+        (skeys[t - 1] == key || jprev != j))
       nofold[q] = 1;
     const int64_t s = q / G.p, b = q - s * G.p;
     const int64_t C = (b + s) % G.p;
-    const int32_t e = perm[t];
-    if (e < 0 || e >= nnz) {
-      atomicOr(err, kErrLayout);
-      continue;
-    }
-    const int32_t j = cols[e];
     const uint32_t lcol = (uint32_t)(j - G.col_start(C));
     const int64_t beg = block_ptr[ql];
     const int64_t pos = stratum_major ? t : wblock_ptr[b * G.p + s] + (t - beg);
