@@ -135,12 +135,14 @@ def test_bound_errors():
         with pytest.raises(bgmf.BgmfError) as ei:
             mdl.bind(U_t.data_ptr(), V_t.data_ptr(), ws_t.data_ptr() + 16,
                      sizes["incore_ws_bytes"], 0, 0, None)
-        assert ei.value.code == bgmf.BGMF_E_ARG
-        # host memory where device memory is needed
+        assert ei.value.code == bgmf.BGMF_E_ARG and "256-byte" in str(ei.value)
+        # pageable host memory (256-byte aligned) where device memory is needed
+        host = np.zeros(w.U0.size + 64, dtype=np.float32)
+        off = (-host.ctypes.data % 256) // 4
         with pytest.raises(bgmf.BgmfError) as ei:
-            mdl.bind(w.U0.ctypes.data, V_t.data_ptr(), ws_t.data_ptr(),
+            mdl.bind(host[off:].ctypes.data, V_t.data_ptr(), ws_t.data_ptr(),
                      sizes["incore_ws_bytes"], 0, 0, None)
-        assert ei.value.code == bgmf.BGMF_E_ARG
+        assert ei.value.code == bgmf.BGMF_E_ARG and "device memory" in str(ei.value)
         # a workspace below the block tables
         with pytest.raises(bgmf.BgmfError) as ei:
             mdl.bind(U_t.data_ptr(), V_t.data_ptr(), ws_t.data_ptr(), 64, 0, 0, None)
@@ -170,13 +172,19 @@ def test_streamed_load_groups_bit_exact_and_within_budget(budget_kib):
     ratings); block_ptr and perm equal the oracle's, two epochs equal the
     in-core run bit for bit, and the load's device memory for ratings peaks
     within the budget, or, when the budget is below it, within the bytes
-    needed to bucket the largest block with the smallest batch."""
+    needed to bucket the largest block with the smallest batch.  A budget
+    below two strata is refused with BGMF_E_BUDGET."""
     w = make_config("large", n=48_000, m=1_800, nnz=1_000_000, p=64)
     budget = budget_kib * 1024
     bp_ref, perm_ref = oracle.bucket(w.n, w.m, w.p, w.rows, w.cols)
     widest = int(np.diff(bp_ref[:: w.p]).max())
     if 2 * (widest + 256) * 8 > budget:
-        pytest.skip("budget below two strata")
+        # the ring needs two strata on the device: below that, a clear error
+        from paper_2304_13724_amd import bgmf
+        with pytest.raises(bgmf.BgmfError) as ei:
+            _owned(w, 1, budget=budget)
+        assert ei.value.code == bgmf.BGMF_E_BUDGET and "two strata" in str(ei.value)
+        return
     inc = _owned(w, 2)
     ooc = _owned(w, 2, budget=budget)
     assert ooc[5]["slots"] in (2, 3)
