@@ -24,7 +24,10 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
-SWEEP_SRC = os.path.join(ROOT, "paper_2304_13724_amd", "csrc", "bgmf_sgd.hip")
+# the sources the sweep kernel is compiled from (its traffic figures hold
+# only for the kernel they were measured on)
+SWEEP_SRCS = [os.path.join(ROOT, "paper_2304_13724_amd", "csrc", f)
+              for f in ("bgmf_sgd.hip", "bgmf_internal.h")]
 TRAFFIC_JSON = os.path.join(ROOT, "profiles", "sgd_large_k64_p1024_traffic.json")
 METRIC = "SGD rating updates/sec per epoch + achieved HBM GB/s (k=64, 100M ratings)"
 
@@ -92,9 +95,12 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def _sha1(path):
+def _sweep_sha1():
     import hashlib
-    return hashlib.sha1(open(path, "rb").read()).hexdigest()
+    h = hashlib.sha1()
+    for path in SWEEP_SRCS:
+        h.update(open(path, "rb").read())
+    return h.hexdigest()
 
 
 # how each synthetic workload is drawn (workloads/synth.py)
@@ -281,7 +287,7 @@ def main():
         sweep = [v for k, v in summ["kernels"].items() if "k_sgd_lds" in k]
         res = {"kernel": "k_sgd_lds (one launch = one epoch)", "nnz": int(args.nnz or 100_000_000),
                "bytes_per_launch": sweep[0]["bytes"] if sweep else None,
-               "sweep_source_sha1": _sha1(SWEEP_SRC), "summary": summ}
+               "sweep_source_sha1": _sweep_sha1(), "summary": summ}
         print(json.dumps(res, indent=1))
         return
     if args.gpus != 1:
@@ -369,7 +375,7 @@ def main():
     traffic = None
     if args.traffic and os.path.exists(args.traffic):
         tr = json.load(open(args.traffic))
-        if tr.get("sweep_source_sha1") == _sha1(SWEEP_SRC) and tr.get("nnz") == w.nnz:
+        if tr.get("sweep_source_sha1") == _sweep_sha1() and tr.get("nnz") == w.nnz:
             traffic = tr.get("bytes_per_launch")
     variant = None
     if args.variant_steps > 0 and args.balanced_cuts == 0:

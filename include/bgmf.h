@@ -68,7 +68,7 @@ typedef struct bgmf bgmf_t; /* opaque handle */
  * (Algorithm 1's I = J = p).  Allocates U (n x k) and V (m x k) on the
  * current HIP device.
  *   1 <= n, m < 2^31;  k a multiple of 16 in [16, 256];
- *   1 <= p <= min(n, m, 8192);  ceil(n/p) <= 65536;  ceil(m/p) <= 16384.
+ *   1 <= p <= min(n, m, 8192);  ceil(n/p) <= 65536;  ceil(m/p) <= 65536.
  * Returns NULL on error; the reason is bgmf_last_error(NULL) (per thread). */
 bgmf_t *bgmf_create(int64_t n, int64_t m, int32_t k, int32_t p);
 
@@ -167,7 +167,7 @@ int bgmf_rmse(bgmf_t *h, double *out);
  * same for columns.  bgmf_set_cuts replaces them by caller-given cut points
  * (row_cuts, col_cuts: p + 1 values each, host memory, strictly increasing
  * from 0 to n, resp. m; row-blocks at most 65536 rows, column-blocks at most
- * 16384 columns wide, else BGMF_E_ARG): row i is then in the block R with
+ * 65536 columns wide, else BGMF_E_ARG): row i is then in the block R with
  * row_cuts[R] <= i < row_cuts[R+1].  Strata, the order inside a block and
  * the update are unchanged.  Blocks of unequal size are the paper's
  * suggested extension (Section 3); balanced blocks shorten the serial

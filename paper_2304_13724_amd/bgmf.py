@@ -292,7 +292,7 @@ def bgmf_get_cuts(h, p: int):
 
 
 def bgmf_balanced_cuts(n: int, m: int, p: int, rows, cols, max_rows: int = 65536,
-                       max_cols: int = 16384):
+                       max_cols: int = 65536):
     rows = np.ascontiguousarray(rows, dtype=np.int32)
     cols = np.ascontiguousarray(cols, dtype=np.int32)
     r = np.empty(p + 1, dtype=np.int64)

@@ -8,13 +8,13 @@ namespace bgmfk {
 
 // ---------------------------------------------------------------------------
 // Rating record (8 bytes), stored contiguously per row-block ("wave stream"):
-//   .x = local row (16 bits) | local column << 16 (14 bits) | flags (2 bits)
+//   .x = local row (16 bits) | local column << 16 (16 bits)
 //   .y = rating value (fp32 bits)
 // Local indices are relative to the block's first row / first column.
 // ---------------------------------------------------------------------------
 constexpr int kRowBits = 16;
 constexpr int kColShift = 16;
-constexpr int kColBits = 14;
+constexpr int kColBits = 16;
 constexpr uint32_t kRowMask = (1u << kRowBits) - 1u;
 constexpr uint32_t kColMask = (1u << kColBits) - 1u;
 #ifndef BGMF_PREFETCH

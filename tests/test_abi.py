@@ -33,6 +33,11 @@ def test_library_exports_every_declared_symbol():
     (10, 10, 16, 0, "p must be"),
     (10, 5, 16, 6, "p must be"),
     (10_000_000, 10, 16, 10, "blocks too large"),
+    # one past the widest block a record can index (65,536 local rows or columns)
+    (65_537, 10, 16, 1, "blocks too large"),
+    (10, 65_537, 16, 1, "blocks too large"),
+    (131_073, 131_072, 16, 2, "blocks too large"),
+    (131_072, 131_073, 16, 2, "blocks too large"),
 ])
 def test_create_rejects_bad_shapes(n, m, k, p, needle):
     from paper_2304_13724_amd import bgmf

@@ -40,6 +40,8 @@ CASES = {
     "duplicates": lambda: _uniform(200, 150, 20_000, 16, 7, 10, dup=True),
     "single_rating": lambda: _uniform(10, 10, 1, 16, 3, 11),
     "ragged_p": lambda: _uniform(1_003, 997, 40_000, 32, 13, 12),
+    # the widest blocks a record can index: 65,536 rows by 65,536 columns
+    "widest_blocks": lambda: _uniform(131_072, 131_072, 300_000, 16, 2, 13),
 }
 
 

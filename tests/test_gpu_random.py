@@ -43,7 +43,7 @@ def _draw(seed):
     if rng.random() < 0.4 and p > 1:
         rc = np.r_[0, np.sort(rng.choice(np.arange(1, n), p - 1, replace=False)), n]
         cc = np.r_[0, np.sort(rng.choice(np.arange(1, m), p - 1, replace=False)), m]
-        if np.diff(cc).max() <= 16384:
+        if np.diff(cc).max() <= 65536:
             cuts = (rc.astype(np.int64), cc.astype(np.int64))
     opts = dict(
         passes=int(rng.choice([1, 1, 2])),
