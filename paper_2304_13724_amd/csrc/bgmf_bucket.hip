@@ -234,12 +234,27 @@ k_radix_scatter(const uint64_t *__restrict__ kin, const int32_t *__restrict__ vi
 
 // ----------------------------------------------------------------- layout
 
+// Ratings per slot, from the sorted keys: a slot's ratings are the run
+// [start, end) of equal slots, so the first rating of each run subtracts its
+// position from its slot's count and adds it to the count of the run before
+// (whose end it is), and the last rating adds nnz: two atomics per occupied
+// slot instead of one per rating (counts start at 0; the arithmetic wraps
+// modulo 2^64 and ends at end - start).  Keys of out-of-range slots sort
+// last and raise the layout error.
 __global__ void k_slot_count(const uint64_t *__restrict__ keys, int64_t nnz, int rbits,
                              int64_t slots, unsigned long long *__restrict__ count, int32_t *err) {
-  for (int64_t e = gid(); e < nnz; e += (int64_t)gridDim.x * blockDim.x) {
-    const uint64_t q = keys[e] >> rbits;
-    if (q < (uint64_t)slots) atomicAdd(&count[q], 1ull);
-    else atomicOr(err, kErrLayout);
+  for (int64_t t = gid(); t < nnz; t += (int64_t)gridDim.x * blockDim.x) {
+    const uint64_t q = keys[t] >> rbits;
+    if (q >= (uint64_t)slots) {
+      atomicOr(err, kErrLayout);
+      continue;
+    }
+    const uint64_t qp = t > 0 ? keys[t - 1] >> rbits : ~0ull;
+    if (q != qp) {
+      atomicAdd(&count[q], 0ull - (unsigned long long)t);
+      if (qp < (uint64_t)slots) atomicAdd(&count[qp], (unsigned long long)t);
+    }
+    if (t == nnz - 1) atomicAdd(&count[q], (unsigned long long)nnz);
   }
 }
 
