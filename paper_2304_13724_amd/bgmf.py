@@ -9,6 +9,7 @@ from __future__ import annotations
 import ctypes
 import math
 import os
+import sys
 
 import numpy as np
 
@@ -335,6 +336,10 @@ class Model:
             self.h = None
 
     def __del__(self):
+        # at interpreter shutdown the HIP runtime may already be torn down:
+        # leave the handle to the process exit instead of calling into it
+        if sys.is_finalizing():
+            return
         try:
             self.close()
         except Exception:
