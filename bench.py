@@ -208,7 +208,8 @@ CPU_THREADS_MAX = 16
 def cpu_baseline(w, threads=None, layout=None):
     """Time the CPU oracle on one whole epoch of the same workload (its
     blocked epoch: every stratum, every block), multithreaded or on one
-    thread.  Returns (result, layout)."""
+    thread, from the initial factors.  Returns (result, layout, (U, V)):
+    the oracle's bucketing and its factors after the epoch."""
     import oracle
 
     info = host_info()
@@ -232,7 +233,48 @@ def cpu_baseline(w, threads=None, layout=None):
         "epoch_s": dt,
     }
     res.update(info)
-    return res, (bp, perm)
+    return res, (bp, perm), (U, V)
+
+
+def _row_rel_err(a, b):
+    """max over rows of |a_i - b_i|_inf / |b_i|_inf."""
+    import numpy as np
+    num = np.abs(a.astype(np.float64) - b).max(axis=1)
+    den = np.abs(b.astype(np.float64)).max(axis=1)
+    return float((num / np.where(den > 0, den, 1.0)).max())
+
+
+def full_size_parity(mdl, w, layout, Uo, Vo, threads):
+    """The GPU's first epoch from the initial factors against the oracle's
+    epoch of the CPU baseline, on the whole benchmark workload: the layout
+    bit for bit, U and V (row-normwise relative error) and the RMSE after
+    the epoch.  The oracle's RMSE is summed over slices on the host's
+    threads and combined in binary64."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    import numpy as np
+    import oracle
+
+    bp, perm = mdl.get_layout()
+    layout_equal = bool(np.array_equal(bp, layout[0]) and np.array_equal(perm, layout[1]))
+    mdl.set_factors(w.U0, w.V0)
+    mdl.epoch(w.alpha, w.beta)
+    r_gpu = mdl.rmse()
+    U, V = mdl.get_factors()
+    step = -(-w.nnz // (4 * threads))
+    spans = [(a, min(a + step, w.nnz)) for a in range(0, w.nnz, step)]
+
+    def part(span):
+        a, b = span
+        return (b - a) * oracle.rmse(w.rows[a:b], w.cols[a:b], w.vals[a:b], Uo, Vo) ** 2
+
+    with ThreadPoolExecutor(max_workers=threads) as ex:
+        r_or = float(np.sqrt(sum(ex.map(part, spans)) / w.nnz))
+    return {"layout_bit_exact": layout_equal,
+            "u_row_rel_err_epoch1": _row_rel_err(U, Uo),
+            "v_row_rel_err_epoch1": _row_rel_err(V, Vo),
+            "rmse_rel_err_epoch1": abs(r_gpu - r_or) / r_or,
+            "rmse_epoch1": r_gpu, "rmse_epoch1_oracle": r_or, "tolerance": 1e-4}
 
 
 def chain_model(stream):
@@ -458,11 +500,17 @@ def main():
         log(f"trace: {trace_summary}")
     t_dep, copy_gbs = chain_model(stream) if args.model else (None, None)
     cpu = None
+    parity = None
     if args.cpu:
-        cpu, layout = cpu_baseline(w)
+        cpu, layout, (Uo, Vo) = cpu_baseline(w)
         log(f"cpu baseline: {cpu['sample']}")
+        if args.balanced_cuts == 0 and args.passes == 1:
+            # after the timed region: the GPU's epoch from the same start
+            parity = full_size_parity(mdl, w, layout, Uo, Vo, cpu["cores"])
+            log(f"parity at full size: {parity}")
+        del Uo, Vo
         if args.cpu_one_thread:
-            one, _ = cpu_baseline(w, threads=1, layout=layout)
+            one, _, _ = cpu_baseline(w, threads=1, layout=layout)
             cpu["value_1_thread"] = one["value"]
             cpu["epoch_s_1_thread"] = one["epoch_s"]
             cpu["sample"] += (f"; the same epoch on one thread (the paper's CMF analogue): "
@@ -501,6 +549,7 @@ def main():
             "bytes_per_update": b_alg,
         },
         "cpu_baseline": cpu,
+        "parity": parity,
         "balanced_blocks_variant": variant,
         "reordered_variant": reordered,
         "sweep_ms": sweep_avg,
