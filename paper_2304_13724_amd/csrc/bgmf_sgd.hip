@@ -949,9 +949,130 @@ __global__ void __launch_bounds__(256) k_sgd_gv(SgdParams P) {
         decode(Wn1, c + CH);
         Wn1 = Wn2;
       };
+      // One float per lane (k <= 64): the same step with the stores of a
+      // rating's results deferred into the next rating's reduction and every
+      // independent instruction pinned between the reduction levels, as in
+      // the LDS sweep.  A rating's global stores then come after the
+      // prefetch issued in its own step (the prefetch of the rating D later),
+      // so the lookup reaches one rating further back (ratings t - 15 ..
+      // t - 1 of the next one); its LDS ring entry is written, like its
+      // stores, at the start of the next step, before that step's lookup.
+      // The arithmetic is unchanged: the results are the same bits.  (With
+      // two or more floats per lane the extra stores and loads overfill the
+      // gaps, and the compiler's order is faster.)
+      //   u, vv: operands of the current rating (chosen at the end of the
+      //   step before); pnu, pnv, prow, pcol: results of the previous rating
+      //   and where they go; x64: x / KPL of the current rating
+      float pnu[NV], pnv[NV], u[NV], vv[NV];
+      uint32_t prow = ringrow[0], pcol = rl(wcol, CH);
+      uint32_t ccur_p = pcol;
+      float x64 = __uint_as_float(rl(__float_as_uint(wx), CH));
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        u[v] = ring[0][v];
+        vv[v] = vring[0][v];
+        pnu[v] = u[v];  // rating 0's current u and v, written back unchanged
+        pnv[v] = vv[v];
+      }
+      auto chunk_pinned = [&](auto tail_tag, int32_t c) {
+        constexpr bool TAIL = decltype(tail_tag)::value;
+        const int32_t left = TAIL ? tail_left(len, c) : CH;
+        const uint2 Wn2 = rp[c + CH + lane];
+#pragma unroll
+        for (int j = 0; j < CH; ++j) {
+          const int next = (j + 1) % D;  // ring slot of the next rating
+          const uint32_t row = ringrow[j];
+          float vl[NV], du[NV], dv[NV];
+          float t = fmaf(-u[0], vv[0], x64);
+#pragma unroll
+          for (int v = 1; v < NV; ++v) t = fmaf(-u[v], vv[v], t);
+          pin();
+          st_row<NV, 0>(pnu, Ures, doff, prow);
+          pin();
+          t = t + dpp_mov<0xB1>(t);  // quad_perm [1,0,3,2]
+          pin();
+          st_row<NV, VPOL>(pnv, Vres, doff, pcol);
+          lds_st<NV>(pnv, ldsb, rbase + (uint32_t)((j + D - 1) % D) * slotbytes);
+          pin();
+          t = t + dpp_mov<0x4E>(t);  // quad_perm [2,3,0,1]
+          pin();
+          // the next rating's column and x; the row and column of rating
+          // t + D, prefetched below (lane j + 2 CH)
+          const uint32_t col1 = rl(wcol, CH + j + 1);
+          const float x64n = __uint_as_float(rl(__float_as_uint(wx), CH + j + 1));
+          ringrow[j] = rl(wrow, 2 * CH + j);
+          const uint32_t pfcol = rl(wcol, 2 * CH + j);
+          pin();
+          t = t + dpp_mov<0x141>(t);  // row_half_mirror
+          pin();
+          // latest of ratings t-15 .. t-1 (lanes j+1 .. j+15) with the next
+          // rating's column; hit bits are >= 2, so "| 1" gives slot 0 (a
+          // read whose value is not used) when there is none
+          const uint32_t kMask = ((1u << (D - 1)) - 1u) << (j + 1);
+          const uint32_t hit = (uint32_t)__builtin_amdgcn_ballot_w64(wcol == col1) & kMask;
+          const uint32_t hslot = (uint32_t)(31 - __builtin_clz(hit | 1u)) & (D - 1);
+          pin();
+          t = t + dpp_mov<0x140>(t);  // row_mirror
+          pin();
+          lds_ld<NV>(vl, ldsb, rbase + hslot * slotbytes);
+#pragma unroll
+          for (int v = 0; v < NV; ++v) {
+            du[v] = nab * u[v];
+            dv[v] = nab * vv[v];
+          }
+          pin();
+          if constexpr (KPL >= 32) t = t + dpp_mov<0x142>(t);  // row_bcast:15
+          pin();
+          // prefetch u and v of rating t + D into slot j
+          ld_row<NV, 0>(ring[j], Ures, doff, ringrow[j]);
+          ld_row<NV, VPOL>(vring[j], Vres, doff, pfcol);
+          const bool same_row = ringrow[next] == row;
+          const bool same_col = col1 == ccur_p;
+          const bool any_hit = hit != 0u;
+          pin();
+          if constexpr (KPL >= 64) t = t + dpp_mov<0x143>(t);  // row_bcast:31
+          pin();
+          const float e = __uint_as_float(rl(__float_as_uint(t), 63));
+          pin();
+          // the next rating's v unless it is this rating's column (in the
+          // wait states of the lane read)
+          float vc[NV];
+#pragma unroll
+          for (int v = 0; v < NV; ++v) vc[v] = any_hit ? vl[v] : vring[next][v];
+          pin();
+          const float ae = alpha * e;
+#pragma unroll
+          for (int v = 0; v < NV; ++v) {
+            const float nu = u[v] + fmaf(ae, vv[v], du[v]);
+            const float nv = vv[v] + fmaf(ae, u[v], dv[v]);
+            pnu[v] = nu;
+            pnv[v] = nv;
+            u[v] = same_row ? nu : ring[next][v];
+            vv[v] = same_col ? nv : vc[v];
+          }
+          prow = row;
+          pcol = ccur_p;
+          ccur_p = col1;
+          x64 = x64n;
+          pin();
+          if constexpr (TAIL) {
+            if (j + 1 >= left) break;  // the block's last rating is done
+          }
+        }
+        decode(Wn1, c + CH);
+        Wn1 = Wn2;
+      };
       const int32_t full = len & ~(CH - 1);
-      for (int32_t c = 0; c < full; c += CH) chunk(std::false_type{}, c);
-      if (full < len) chunk(std::true_type{}, full);
+      if constexpr (NV == 1) {
+        for (int32_t c = 0; c < full; c += CH) chunk_pinned(std::false_type{}, c);
+        if (full < len) chunk_pinned(std::true_type{}, full);
+        // the last rating's results
+        st_row<NV, 0>(pnu, Ures, doff, prow);
+        st_row<NV, VPOL>(pnv, Vres, doff, pcol);
+      } else {
+        for (int32_t c = 0; c < full; c += CH) chunk(std::false_type{}, c);
+        if (full < len) chunk(std::true_type{}, full);
+      }
       }
     }
     if (P.trace) trace_mark(P.trace, 2 * ((int64_t)s * P.p + b) + 1, lane);
