@@ -73,6 +73,39 @@ def test_oracle_parity(case):
         assert abs(x - y) <= TOL * y
 
 
+def _cycle(d, k, reps=40, p=1):
+    """One rating per row, rows ascending, columns cycling through d values:
+    inside a block every column comes back after exactly d ratings (d = 1:
+    one column throughout).  With p = 1 the whole matrix is one block."""
+    from workloads.synth import Workload, init_factors
+    n = d * reps + 3
+    rows = np.arange(n, dtype=np.int32)
+    cols = (rows % d).astype(np.int32)
+    vals = (1 + rows % 5).astype(np.float32)
+    U0, V0 = init_factors(n, max(d, 2), k, 300 + d)
+    return Workload("cycle", n, max(d, 2), k, p, 0.01, 0.05, 1, rows, cols, vals, U0, V0)
+
+
+@pytest.mark.parametrize("k", [64, 128])
+@pytest.mark.parametrize("d", [1, 2, 3, 13, 14, 15, 16, 17, 31])
+def test_repeat_distance(d, k):
+    """A column repeated at exactly distance d.  A rating's v row is
+    prefetched 16 ratings ahead, so it misses the updates of the ratings in
+    between: at k = 128 those at distance 1..15 (a rating's store precedes
+    the prefetch issued in its step), at k <= 64 those at 1..16 (the store
+    is deferred into the next step).  The latest result must replace the
+    prefetch there, and the prefetch is used as loaded beyond: d = 15, 16
+    and 17 are the edges."""
+    w = _cycle(d, k)
+    a = gpu_run(w, 2, v_staging=LDS, single=0)
+    g = gpu_run(w, 2, v_staging=GLOBAL)
+    assert np.array_equal(g[0], a[0]) and np.array_equal(g[1], a[1])
+    U_ref, V_ref, hist_ref, _, _ = oracle_run(w, 2)
+    assert row_rel_err(g[0], U_ref) <= TOL and row_rel_err(g[1], V_ref) <= TOL
+    for x, y in zip(g[2], hist_ref):
+        assert abs(x - y) <= TOL * y
+
+
 def test_placement_option():
     from paper_2304_13724_amd import bgmf
     w = CASES["medium_shape"]()
