@@ -33,7 +33,11 @@ def _oracle_fit(w, rows, cols, vals, max_epochs, delta):
     return U, V, hist
 
 
-def test_fit_matches_oracle_loop():
+@pytest.mark.parametrize("streamed", [False, True])
+def test_fit_matches_oracle_loop(streamed):
+    """The outer loop against the oracle's; streamed: the same run with the
+    ratings streamed from host memory under a budget of two strata plus a
+    margin (the epochs and RMSE passes stream every time)."""
     w = make_config("tiny")
     delta = 0.02
     U_ref, V_ref, hist_ref = _oracle_fit(w, w.rows, w.cols, w.vals, 30, delta)
@@ -43,8 +47,13 @@ def test_fit_matches_oracle_loop():
     assert (d[:-1] > delta * 1.005).all() and d[-1] < delta * 0.995, d
     from paper_2304_13724_amd import bgmf
     with bgmf.Model(w.n, w.m, w.k, w.p) as mdl:
+        if streamed:
+            bp, _ = oracle.bucket(w.n, w.m, w.p, w.rows, w.cols)
+            widest = int(np.diff(bp[:: w.p]).max())
+            mdl.set_option(bgmf.BGMF_OPT_RATINGS_BUDGET, 2 * (widest + 256) * 8 + 4096)
         mdl.set_factors(w.U0, w.V0)
         mdl.load_coo(w.rows, w.cols, w.vals)
+        assert (mdl.get_option(bgmf.BGMF_OPT_STREAM_SLOTS) > 0) == streamed
         ran, hist = mdl.fit(w.alpha, w.beta, 30, delta)
         U, V = mdl.get_factors()
     assert ran == len(hist_ref) - 1
