@@ -68,6 +68,18 @@ def test_one_epoch_parity(case, schedule):
     assert abs(hist[0] - hist_ref[0]) <= TOL * hist_ref[0]
 
 
+def test_largest_grid():
+    """p = 8192, the largest grid: 67M block slots, 8192 strata, mostly
+    empty blocks; bucketing bit-exact and one epoch against the oracle."""
+    w = _uniform(16_384, 16_384, 200_000, 16, 8192, 14)
+    bp_ref, perm_ref = oracle.bucket(w.n, w.m, w.p, w.rows, w.cols)
+    U_ref, V_ref, hist_ref, _, _ = oracle_run(w, 1, layout=(bp_ref, perm_ref))
+    U, V, hist, bp, perm = gpu_run(w, 1)
+    assert np.array_equal(bp, bp_ref) and np.array_equal(perm, perm_ref)
+    assert row_rel_err(U, U_ref) <= TOL and row_rel_err(V, V_ref) <= TOL
+    assert abs(hist[0] - hist_ref[0]) <= TOL * hist_ref[0]
+
+
 @pytest.mark.parametrize("k", [16, 32, 48, 64, 80, 128, 256])
 def test_factor_widths(k):
     w = make_config("medium", n=3_000, m=700, nnz=60_000, p=16, k=k)
