@@ -42,6 +42,10 @@ CASES = {
     "ragged_p": lambda: _uniform(1_003, 997, 40_000, 32, 13, 12),
     # the widest blocks a record can index: 65,536 rows by 65,536 columns
     "widest_blocks": lambda: _uniform(131_072, 131_072, 300_000, 16, 2, 13),
+    # degenerate shapes: a 1 x 1 matrix, one user, one item
+    "one_cell": lambda: _uniform(1, 1, 1, 16, 1, 15),
+    "one_row": lambda: _uniform(1, 500, 400, 32, 1, 16),
+    "one_column": lambda: _uniform(500, 1, 400, 32, 1, 17),
 }
 
 
