@@ -401,12 +401,24 @@ k_rmse_lds(const uint2 *__restrict__ rec, const int64_t *__restrict__ wblock_ptr
   if (lane == 0) partials[(int64_t)b * kLdsWaves + wave] = acc;
 }
 
+// Sum of the partials in a fixed order (the result does not depend on
+// scheduling): thread t adds partials t, t + 256, ... into eight sums by
+// index (eight loads in flight instead of one), combined pairwise, then a
+// tree over the threads.
 __global__ void __launch_bounds__(256)
 k_rmse_final(const double *__restrict__ partials, int64_t count, int64_t nnz, double *out) {
   __shared__ double sh[256];
-  double a = 0.0;
-  for (int64_t i = threadIdx.x; i < count; i += 256) a += partials[i];
-  sh[threadIdx.x] = a;
+  constexpr int A = 8;
+  double a[A];
+#pragma unroll
+  for (int u = 0; u < A; ++u) a[u] = 0.0;
+  int64_t i = threadIdx.x;
+  for (; i + (A - 1) * 256 < count; i += A * 256) {
+#pragma unroll
+    for (int u = 0; u < A; ++u) a[u] += partials[i + u * 256];
+  }
+  for (; i < count; i += 256) a[0] += partials[i];
+  sh[threadIdx.x] = ((a[0] + a[1]) + (a[2] + a[3])) + ((a[4] + a[5]) + (a[6] + a[7]));
   __syncthreads();
   for (int off = 128; off > 0; off >>= 1) {
     if ((int)threadIdx.x < off) sh[threadIdx.x] += sh[threadIdx.x + off];
